@@ -1,0 +1,213 @@
+#!/usr/bin/env python3
+"""Benchmark of one DeDLOC averaging step on one MI355X.
+
+A step is one pass of the whole path over one batch of synthetic input:
+shard bounds on the host, the local peer's encode of its own fp32 gradient
+(the sender side), and the round: every shard averaged from the N peer
+messages, the average re-encoded and gathered, and one LAMB step with
+per-tensor trust ratios over the whole parameter vector.
+
+Default workload: ALBERT-large-shaped (17.7M parameters in 25 tensors,
+16 peers, fp16 wire).  Prints ONE JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E
+
+
+def _parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="albert_large")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-reps", type=int, default=2)
+    return ap.parse_args()
+
+
+def kernel_roofline(dr, prof, steps):
+    """Achieved algorithmic HBM bandwidth of the kernel that dominates the
+    step.  Algorithmic bytes per launch (b = wire bytes per element,
+    N = active peers, P elements):
+      lamb_a_fused_fp16: N*b*P peer reads + b*P code writes + 12P reads of
+                         x, m, v + 8P writes of m', v'
+      reduce_i8:         N*b*P peer reads + b*P code/scale writes
+      lamb_a_i8:         b*P code reads + 20P (x, m, v reads; m', v' writes)
+      lamb_b:            12P reads (x, m', v') + 4P writes
+      encode_fp16 / encode_i8: 4P reads + b*P writes"""
+    wl = dr.wl
+    P = wl.P
+    b = wl.wire_bytes_per_elem
+    n_act = int(np.count_nonzero(dr.counts))
+    per_launch = {
+        "lamb_a_fused_fp16": (n_act * b + b + 20.0) * P,
+        "reduce_i8": (n_act * b + b) * P,
+        "lamb_a_i8": (b + 20.0) * P,
+        "lamb_a_fp16": (b + 20.0) * P,
+        "lamb_b": 16.0 * P,
+        "encode_fp16": (4.0 + b) * P,
+        "encode_i8": (4.0 + b) * P,
+    }
+    name = max(prof, key=lambda k: prof[k][0])
+    total_ms, launches = prof[name]
+    per_step = launches / steps
+    avg_ms = total_ms / launches
+    # chunked kernels launch several times per step; bytes per launch scale
+    nbytes = per_launch.get(name, 0.0) / per_step
+    achieved = nbytes / (avg_ms * 1e-3) / 1e9
+    return name, {
+        "bound": "hbm",
+        "kernel": name,
+        "achieved": round(achieved, 1),
+        "peak": HBM_PEAK_GBPS,
+        "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBPS, 4),
+        "traffic": None,
+        "avg_launch_us": round(avg_ms * 1e3, 2),
+        "algorithmic_bytes_per_launch": nbytes,
+    }, {k: {"ms_per_step": round(v[0] / steps, 4), "launches_per_step": v[1] / steps} for k, v in prof.items()}
+
+
+def cpu_baseline(wl, dr, reps):
+    """The oracle (plain sequential C) on the same workload: one local encode
+    plus one round, on the host, timed after its inputs are prepared."""
+    import torch
+    import oracle
+    from paper_2106_10207_amd import workloads as W
+    oracle.build(force=False)
+    codec = 1 if wl.codec == "fp16" else 2
+    codes, scales = [], []
+    local_grad = None
+    for p in range(wl.n_peers):
+        g = W.peer_gradient(wl, p, "cuda").cpu().numpy()
+        if codec == 1:
+            codes.append(oracle.encode_fp16(g))
+        else:
+            c, s = oracle.encode_i8(g, 1024)
+            codes.append(c)
+            scales.append(s)
+        if p == dr.local:
+            local_grad = g
+        del g
+    x, m, v = (t.cpu().numpy() for t in W.optimizer_state(wl, "cuda"))
+    cfg = oracle.lamb_cfg(wl.lr, wl.beta1, wl.beta2, wl.eps, wl.weight_decay, step=wl.step)
+    bw = W.bandwidth_weights(wl)
+    times = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        bounds = oracle.partition(wl.P, wl.n_shards, bw, wl.shard_align)
+        if codec == 1:
+            oracle.encode_fp16(local_grad)
+        else:
+            oracle.encode_i8(local_grad, 1024)
+        oracle.round_(codes, dr.counts, bounds, codec, x, m, v, wl.offsets(), wl.flags(), cfg,
+                      scales or None, 1024)
+        times.append(time.perf_counter() - t0)
+    t = float(np.mean(times))
+    return {
+        "value": round(dr.bytes_peer_input() / t / 1e9, 4),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"the full {wl.name} step (partition + local encode + round over all "
+                  f"{wl.P} elements), mean of {reps} runs, single thread",
+        "s_per_step": round(t, 3),
+    }
+
+
+def main():
+    args = _parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2106_10207_amd import dedloc as D
+    from paper_2106_10207_amd import harness as H
+    from paper_2106_10207_amd import workloads as W
+
+    wl = W.WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    D.load()
+    dr = H.DeviceRound(wl, "cuda", keep_local_grad=True)
+    bw = W.bandwidth_weights(wl)
+
+    def step():
+        D.dedloc_partition(wl.P, wl.n_shards, bw, wl.shard_align)
+        dr.encode_local()
+        dr.run()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: K steps bracketed by device synchronisation, HIP events
+    # on the stream every kernel is launched on
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+
+    # same K steps again with per-kernel events (roofline of the dominant kernel)
+    D.dedloc_profile_begin(64 * args.steps + 64)
+    for _ in range(args.steps):
+        step()
+    prof = D.dedloc_profile_end()
+    kname, roof, per_kernel = kernel_roofline(dr, prof, args.steps)
+
+    t = ms_per_step * 1e-3
+    peer_bytes = dr.bytes_peer_input()
+    alg_bytes = dr.bytes_round() + dr.bytes_encode_local()
+    out = {
+        "metric": "reduce+LAMB round GB/s of peer input (fraction of HBM peak); params/s",
+        "value": round(peer_bytes / t / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.name,
+            "params": wl.P,
+            "tensors": wl.n_tensors,
+            "peers": wl.n_peers,
+            "active_peers": int(np.count_nonzero(dr.counts)),
+            "wire": wl.codec,
+            "shards": wl.n_shards,
+            "parallelism": "single GPU; peers are HBM regions",
+        },
+        "params_per_s": round(wl.P / t, 1),
+        "algorithmic_GBps": round(alg_bytes / t / 1e9, 2),
+        "algorithmic_frac_of_peak": round(alg_bytes / t / 1e9 / HBM_PEAK_GBPS, 4),
+        "roofline": roof,
+        "kernels": per_kernel,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, dr, args.cpu_reps)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,211 @@
+/*
+ * dedloc.h - C ABI of the MI355X (gfx950) library for one DeDLOC averaging
+ * round: wire codecs, the per-reducer shard average, and the LAMB step.
+ *
+ * The paper (Distributed Deep Learning In Open Collaborations) averages
+ * gradients by reduce-scatter then all-gather (Section 3.2): every peer is
+ * assigned a share of the flat gradient vector proportional to its
+ * throughput (Appendix B), receives that share from every sender, averages
+ * it and returns the average; after the exchange every peer applies one
+ * optimizer step (Section 3.1), LAMB in the paper's transformer runs.
+ * Here the N peers' messages are N regions of one GPU's memory.
+ *
+ * Conventions for every call below
+ *  - Pointers are DEVICE pointers unless the argument says "host".
+ *  - The caller owns every buffer; the library allocates no device memory.
+ *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = the null
+ *    stream): they validate their arguments on the host, enqueue kernels and
+ *    return.  Invalid arguments are rejected before anything is enqueued and
+ *    leave every output untouched.
+ *  - Return value: DEDLOC_OK (0) or a negative dedloc_status;
+ *    dedloc_last_error() gives a message for the calling thread's last
+ *    failure.  No C++ exception crosses the ABI.
+ *  - fp32 and fp16 buffers are read and written in 16-byte vectors: their
+ *    pointers must be 16-byte aligned (DEDLOC_ERR_ALIGN otherwise), int8
+ *    code buffers too; scale buffers 4-byte aligned.
+ *  - Codec ids: DEDLOC_CODEC_F32 (raw fp32; only as the LAMB gradient),
+ *    DEDLOC_CODEC_FP16, DEDLOC_CODEC_I8 (8-bit absmax; `block` = 1024).
+ *    For fp16 and f32 the `block` argument is ignored.
+ */
+#ifndef DEDLOC_H
+#define DEDLOC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DEDLOC_OK = 0,
+    DEDLOC_ERR_INVALID_ARG = -1,
+    DEDLOC_ERR_ALIGN = -2,
+    DEDLOC_ERR_ZERO_WEIGHT = -3,
+    DEDLOC_ERR_WORKSPACE = -4,
+    DEDLOC_ERR_HIP = -5
+} dedloc_status;
+
+enum { DEDLOC_CODEC_F32 = 0, DEDLOC_CODEC_FP16 = 1, DEDLOC_CODEC_I8 = 2 };
+
+/* Maximum number of peers in one reduce or round call. */
+#define DEDLOC_MAX_PEERS 64
+/* The only supported int8 block length. */
+#define DEDLOC_I8_BLOCK 1024
+
+/* Per-tensor flag bits for the LAMB step. */
+#define DEDLOC_TENSOR_DECAY 1u /* apply weight decay to this tensor */
+#define DEDLOC_TENSOR_ADAPT 2u /* apply the layer-wise trust ratio */
+
+/* LAMB hyper-parameters (host struct). step >= 1 is the 1-based step index
+ * used for bias correction.  force_unit_trust != 0 replaces every trust ratio
+ * by 1 (the step is then AdamW with decoupled weight decay). */
+typedef struct {
+    float lr, beta1, beta2, eps, weight_decay;
+    uint64_t step;
+    int32_t bias_correction;
+    int32_t force_unit_trust;
+} dedloc_lamb_cfg;
+
+/* Library version (major*10000 + minor*100 + patch). */
+int dedloc_version(void);
+
+/* Message for the calling thread's last failed call ("" if none). */
+const char *dedloc_last_error(void);
+
+/* Size of one encoded message of n elements: returns the code bytes and
+ * stores the number of fp32 scales in *n_scales (host, nullable): 0 for
+ * fp16, ceil(n / block) for int8.  Returns 0 for an unknown codec. */
+size_t dedloc_encoded_bytes(int32_t codec, uint32_t block, uint64_t n, uint64_t *n_scales);
+
+/* Shard bounds (host only, integer).  Section 3.2 / Appendix B assign each
+ * aggregating peer a share of the vector proportional to its effective
+ * throughput.  With C_k the sum of the first k weights (weights = NULL means
+ * equal weights):
+ *     bounds[0] = 0, bounds[k] = align * floor(P * C_k / (C_n * align)),
+ *     bounds[n_shards] = P,
+ * so the shards tile [0, P), interior bounds are multiples of `align`, and
+ * the last shard keeps the remainder.  bounds (host) has n_shards+1 entries.
+ * Errors: n_shards == 0, align == 0, all weights zero -> INVALID_ARG. */
+int dedloc_partition(uint64_t P, uint32_t n_shards, const uint64_t *weights,
+                     uint32_t align, uint64_t *bounds);
+
+/* Peer weights (host only).  The averaged gradient is the mean over all
+ * accumulated samples (appendix "Convergence analysis"): peer p, whose mean
+ * gradient covers counts[p] samples, gets w[p] = counts[p] / sum(counts),
+ * one correctly rounded fp32 division.  sum(counts) must be in [1, 2^24].
+ * Errors: all counts zero -> ZERO_WEIGHT; sum above 2^24 -> INVALID_ARG. */
+int dedloc_weights(const uint32_t *counts, uint32_t n, float *w);
+
+/* Encode n fp32 values (the sender's side of the exchange).
+ *   fp16: IEEE binary16, round to nearest even, subnormals kept, overflow
+ *         to infinity.  codes: uint16[n].  scales unused (may be NULL).
+ *   int8: blocks of `block` elements from x[0] (last block partial):
+ *         s = max|x| / 127 (fp32), q = clamp(rint(x/s), -127, 127), ties to
+ *         even; an all-zero block has s = 0 and q = 0.  codes: int8[n],
+ *         scales: float[ceil(n/block)].  Inputs must be finite.
+ * n == 0 is a no-op. */
+int dedloc_encode(const float *x, uint64_t n, int32_t codec, uint32_t block,
+                  void *codes, float *scales, void *stream);
+
+/* Decode n elements: fp16 -> fp32 exactly; int8 -> q * s (one rounding). */
+int dedloc_decode(const void *codes, const float *scales, uint64_t n,
+                  int32_t codec, uint32_t block, float *out, void *stream);
+
+/* The reducer's step (Section 3.2): average one shard of shard_len
+ * elements as sent by n_peers peers and re-encode the average.
+ *   peer_codes  (host array of n_peers device pointers) - each peer's
+ *               message for this shard, already offset to the shard start;
+ *   peer_scales (host array, int8 only; NULL for fp16) - each peer's block
+ *               scales for this shard (blocks counted from the shard start);
+ *   counts      (host, n_peers) - accumulated samples per peer.
+ * mean[e] = sum over peers with counts > 0, in ascending order, of
+ * w_p * decode_p[e], accumulated from +0 with one fused multiply-add per
+ * peer (w_p as in dedloc_weights).  Peers with zero samples are never read
+ * (Appendix B: a peer that does not compute still aggregates, and its local
+ * gradient is disregarded); their pointers may be NULL.
+ * Outputs: out_codes / out_scales - the encoded average (as dedloc_encode);
+ * out_mean (nullable) - the fp32 average before encoding.
+ * Errors: n_peers == 0 or > DEDLOC_MAX_PEERS -> INVALID_ARG; all counts
+ * zero -> ZERO_WEIGHT.  shard_len == 0 is a no-op (after validation). */
+int dedloc_reduce_shard(const void *const *peer_codes, const float *const *peer_scales,
+                        const uint32_t *counts, uint32_t n_peers, uint64_t shard_len,
+                        int32_t codec, uint32_t block, void *out_codes,
+                        float *out_scales, float *out_mean, void *stream);
+
+/* Workspace for dedloc_lamb_step / dedloc_round with this tensor table
+ * (offsets: host, n_tensors+1).  Returns 0 for an invalid table.
+ * The workspace must be zero-filled once before its first use (for example
+ * with dedloc_workspace_clear); every call leaves it in a reusable state.
+ * Calls that share one workspace must not overlap in time. */
+size_t dedloc_lamb_workspace_bytes(uint64_t P, const uint64_t *offsets, uint32_t n_tensors);
+
+/* Zero-fill a workspace with a kernel (no memset node, so it may be
+ * captured into a graph). */
+int dedloc_workspace_clear(void *ws, size_t ws_bytes, void *stream);
+
+/* One LAMB step over a flat parameter buffer (Section 3.1 trains with LAMB;
+ * the sahajBERT-XL appendix keeps its statistics), with the published LAMB
+ * update and a trust ratio per tensor:
+ *   m' = fma(b1, m, (1-b1)*g);  v' = fma(b2, v, (1-b2)*(g*g))
+ *   u  = (m'/c1) / (sqrt(v'/c2) + eps) + lambda_t * x,  c_i = 1 - b_i^step
+ *        (c_i computed in double, rounded to fp32; 1 without bias correction)
+ *   r_t = ||x_t|| / ||u_t||, or 1 if either norm is 0, the tensor lacks
+ *         DEDLOC_TENSOR_ADAPT, or force_unit_trust is set
+ *   x' = x - (lr * r_t) * u
+ * lambda_t = weight_decay if the tensor has DEDLOC_TENSOR_DECAY, else 0.
+ *   x, m, v    fp32[P], updated in place;
+ *   grad       the gradient: fp32[P] (grad_codec = DEDLOC_CODEC_F32) or an
+ *              encoded message of P elements (fp16, or int8 with grad_scales);
+ *   offsets    host uint64[n_tensors+1]: offsets[0] = 0, offsets[T] = P,
+ *              non-decreasing, every offset except P a multiple of 8;
+ *   flags      host uint8[n_tensors];
+ *   trust_out  device float[n_tensors] (nullable): r_t.
+ * The norms are accumulated in fp64 in a fixed order, so results are
+ * deterministic run to run. */
+int dedloc_lamb_step(float *x, float *m, float *v, const void *grad,
+                     const float *grad_scales, int32_t grad_codec, uint32_t block,
+                     uint64_t P, const uint64_t *offsets, const uint8_t *flags,
+                     uint32_t n_tensors, const dedloc_lamb_cfg *cfg, float *trust_out,
+                     void *ws, size_t ws_bytes, void *stream);
+
+/* One whole averaging round as seen by one GPU holding every reducer
+ * (Sections 3.1-3.2): each shard [bounds[k], bounds[k+1]) of the vector is
+ * averaged from the n_peers messages (as dedloc_reduce_shard), the encoded
+ * averages are gathered into out_codes / out_scales (full-vector messages),
+ * and every element is decoded from that gathered message and updated by
+ * one LAMB step (as dedloc_lamb_step).  Fused: the fp16 path reads each
+ * peer byte once and re-reads only x, m and v for the trust ratio.
+ *   peer_codes  host array of n_peers device pointers to full-vector
+ *               messages (P elements); peer_scales likewise for int8;
+ *   bounds      host uint64[n_shards+1] tiling [0, P); for int8 every
+ *               interior bound must be a multiple of `block`;
+ *   out_mean    nullable fp32[P]: the average before encoding.
+ * Workspace as dedloc_lamb_workspace_bytes. */
+int dedloc_round(const void *const *peer_codes, const float *const *peer_scales,
+                 const uint32_t *counts, uint32_t n_peers, const uint64_t *bounds,
+                 uint32_t n_shards, int32_t codec, uint32_t block, void *out_codes,
+                 float *out_scales, float *x, float *m, float *v, uint64_t P,
+                 const uint64_t *offsets, const uint8_t *flags, uint32_t n_tensors,
+                 const dedloc_lamb_cfg *cfg, float *trust_out, float *out_mean,
+                 void *ws, size_t ws_bytes, void *stream);
+
+/* Per-kernel timing (tracing support for benchmarks).  Between
+ * dedloc_profile_begin() and dedloc_profile_end() every kernel the library
+ * enqueues is bracketed by a pair of HIP events on its stream; at most
+ * max_launches launches are recorded (later ones are not timed).
+ * dedloc_profile_end waits for the recorded events and writes, for every
+ * kernel kind k < n_kinds, the summed duration total_ms[k] (host) and the
+ * launch count launches[k] (host).  Kinds are named by
+ * dedloc_kernel_name(k); dedloc_kernel_kinds() gives their number.
+ * Profiling is process-wide; calls from several threads are serialised. */
+int dedloc_profile_begin(uint32_t max_launches);
+int dedloc_profile_end(uint32_t n_kinds, double *total_ms, uint64_t *launches);
+int dedloc_kernel_kinds(void);
+const char *dedloc_kernel_name(int kind);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DEDLOC_H */

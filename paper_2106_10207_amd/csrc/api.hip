@@ -1,0 +1,471 @@
+// C ABI of libdedloc (declared in include/dedloc.h): argument validation,
+// host-side integer work (shard bounds, peer weights, LAMB tile tables) and
+// the launch sequence of each call.  All arithmetic on vector data runs in
+// the kernels of kernels.hip.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/dedloc.h"
+#include "dedloc_internal.h"
+
+using namespace dedloc;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+    return fail(DEDLOC_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// ------------------------------------------------------------ profiling
+enum Kind {
+    K_ENCODE_FP16, K_DECODE_FP16, K_ENCODE_I8, K_DECODE_I8, K_REDUCE_FP16, K_REDUCE_I8,
+    K_LAMB_A_F32, K_LAMB_A_FP16, K_LAMB_A_I8, K_LAMB_A_FUSED_FP16, K_LAMB_B, K_FILL, K_COUNT
+};
+const char *const kKindNames[K_COUNT] = {
+    "encode_fp16", "decode_fp16", "encode_i8", "decode_i8", "reduce_fp16", "reduce_i8",
+    "lamb_a_f32", "lamb_a_fp16", "lamb_a_i8", "lamb_a_fused_fp16", "lamb_b", "fill_zero"};
+
+struct Profiler {
+    std::mutex mu;
+    bool on = false;
+    uint32_t cap = 0;
+    std::vector<hipEvent_t> ev;     // 2 per recorded launch
+    std::vector<int> kind;
+    size_t used = 0;
+} g_prof;
+
+// Run `launch` (returning hipError_t), bracketed by events when profiling.
+template <typename F>
+hipError_t timed(int kind, hipStream_t s, F launch) {
+    std::unique_lock<std::mutex> lk(g_prof.mu);
+    if (!g_prof.on || g_prof.used >= g_prof.cap) {
+        lk.unlock();
+        return launch();
+    }
+    const size_t i = g_prof.used++;
+    while (g_prof.ev.size() < 2 * g_prof.used) {
+        hipEvent_t e;
+        hipError_t r = hipEventCreate(&e);
+        if (r != hipSuccess) return r;
+        g_prof.ev.push_back(e);
+    }
+    g_prof.kind.resize(g_prof.used);
+    g_prof.kind[i] = kind;
+    hipError_t r = hipEventRecord(g_prof.ev[2 * i], s);
+    if (r != hipSuccess) return r;
+    r = launch();
+    if (r != hipSuccess) return r;
+    return hipEventRecord(g_prof.ev[2 * i + 1], s);
+}
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Host copy of dedloc_weights' definition: exact integer total, exactly
+// converted, one fp32 division per peer.
+int compute_weights(const uint32_t *counts, uint32_t n, float *w) {
+    uint64_t W = 0;
+    for (uint32_t p = 0; p < n; p++) W += counts[p];
+    if (W == 0) return fail(DEDLOC_ERR_ZERO_WEIGHT, "every peer has zero samples");
+    if (W > (1u << 24)) return fail(DEDLOC_ERR_INVALID_ARG, "total sample count %llu exceeds 2^24",
+                                    (unsigned long long)W);
+    for (uint32_t p = 0; p < n; p++) w[p] = (float)counts[p] / (float)W;
+    return DEDLOC_OK;
+}
+
+int check_codec(int32_t codec, uint32_t block, bool allow_f32) {
+    if (codec == DEDLOC_CODEC_FP16) return DEDLOC_OK;
+    if (codec == DEDLOC_CODEC_F32 && allow_f32) return DEDLOC_OK;
+    if (codec == DEDLOC_CODEC_I8) {
+        if (block != DEDLOC_I8_BLOCK)
+            return fail(DEDLOC_ERR_INVALID_ARG, "int8 block must be %d (got %u)", DEDLOC_I8_BLOCK, block);
+        return DEDLOC_OK;
+    }
+    return fail(DEDLOC_ERR_INVALID_ARG, "unknown codec %d", codec);
+}
+
+// Active-peer table: peers with counts > 0 in ascending order.
+int build_peers(const void *const *codes, const float *const *scales, const uint32_t *counts,
+                uint32_t n, int32_t codec, PeerTable &pt, bool check_ptrs = true) {
+    if (!codes || !counts) return fail(DEDLOC_ERR_INVALID_ARG, "peer_codes and counts must not be NULL");
+    if (n == 0 || n > DEDLOC_MAX_PEERS)
+        return fail(DEDLOC_ERR_INVALID_ARG, "n_peers must be in [1, %d] (got %u)", DEDLOC_MAX_PEERS, n);
+    if (codec == DEDLOC_CODEC_I8 && !scales)
+        return fail(DEDLOC_ERR_INVALID_ARG, "int8 messages need peer_scales");
+    float w[DEDLOC_MAX_PEERS];
+    int rc = compute_weights(counts, n, w);
+    if (rc) return rc;
+    memset(&pt, 0, sizeof pt);
+    for (uint32_t p = 0; p < n; p++) {
+        if (counts[p] == 0) continue;  // weight 0: never read
+        if (!check_ptrs) continue;     // nothing will be read at all
+        if (!codes[p]) return fail(DEDLOC_ERR_INVALID_ARG, "peer %u has samples but a NULL message", p);
+        if (!aligned(codes[p], 16)) return fail(DEDLOC_ERR_ALIGN, "peer %u message is not 16-byte aligned", p);
+        if (codec == DEDLOC_CODEC_I8) {
+            if (!scales[p]) return fail(DEDLOC_ERR_INVALID_ARG, "peer %u has samples but NULL scales", p);
+            if (!aligned(scales[p], 4)) return fail(DEDLOC_ERR_ALIGN, "peer %u scales not 4-byte aligned", p);
+            pt.scales[pt.n] = scales[p];
+        }
+        pt.codes[pt.n] = codes[p];
+        pt.w[pt.n] = w[p];
+        pt.n++;
+    }
+    return DEDLOC_OK;
+}
+
+// LAMB tile table: tensors in launch chunks of at most kChunkTensors.
+struct Plan {
+    std::vector<Chunk> chunks;
+    std::vector<uint32_t> chunk_tiles;
+    uint32_t n_tiles = 0;
+    size_t ws_partials = 0, ws_counters = 0, ws_trust = 0, ws_total = 0;
+};
+
+int check_tensors(uint64_t P, const uint64_t *off, uint32_t T) {
+    if (!off) return fail(DEDLOC_ERR_INVALID_ARG, "offsets must not be NULL");
+    if (T == 0) return fail(DEDLOC_ERR_INVALID_ARG, "n_tensors must be >= 1");
+    if (off[0] != 0 || off[T] != P)
+        return fail(DEDLOC_ERR_INVALID_ARG, "tensor offsets must start at 0 and end at P");
+    for (uint32_t t = 0; t < T; t++) {
+        if (off[t + 1] < off[t]) return fail(DEDLOC_ERR_INVALID_ARG, "tensor offsets decrease at %u", t);
+        if (off[t] % kVec) return fail(DEDLOC_ERR_ALIGN, "tensor offset %u is not a multiple of 8", t);
+    }
+    return DEDLOC_OK;
+}
+
+void make_plan(uint64_t P, const uint64_t *off, const uint8_t *flags, uint32_t T, Plan &pl) {
+    (void)P;
+    pl.chunks.clear();
+    pl.chunk_tiles.clear();
+    uint32_t base = 0;
+    for (uint32_t t0 = 0; t0 < T; t0 += kChunkTensors) {
+        Chunk c;
+        memset(&c, 0, sizeof c);
+        c.nt = (T - t0 < (uint32_t)kChunkTensors) ? T - t0 : kChunkTensors;
+        c.t0 = t0;
+        c.tile_base = base;
+        uint32_t tiles = 0;
+        for (uint32_t k = 0; k < c.nt; k++) {
+            c.off[k] = off[t0 + k];
+            c.tile_begin[k] = tiles;
+            c.flags[k] = flags ? flags[t0 + k] : 0;
+            const uint64_t len = off[t0 + k + 1] - off[t0 + k];
+            tiles += (uint32_t)((len + kTile - 1) / kTile);
+        }
+        c.off[c.nt] = off[t0 + c.nt];
+        c.tile_begin[c.nt] = tiles;
+        pl.chunks.push_back(c);
+        pl.chunk_tiles.push_back(tiles);
+        base += tiles;
+    }
+    pl.n_tiles = base;
+    pl.ws_partials = round_up((size_t)base * 2 * sizeof(double), 256);
+    pl.ws_counters = round_up((size_t)T * sizeof(unsigned), 256);
+    pl.ws_trust = round_up((size_t)T * sizeof(float), 256);
+    pl.ws_total = pl.ws_partials + pl.ws_counters + pl.ws_trust;
+}
+
+LambWs carve(const Plan &pl, void *ws) {
+    char *b = (char *)ws;
+    LambWs w;
+    w.partials = (double *)b;
+    w.counters = (unsigned *)(b + pl.ws_partials);
+    w.trust = (float *)(b + pl.ws_partials + pl.ws_counters);
+    return w;
+}
+
+int make_params(const dedloc_lamb_cfg *cfg, LambParams &lp) {
+    if (!cfg) return fail(DEDLOC_ERR_INVALID_ARG, "cfg must not be NULL");
+    if (cfg->step == 0) return fail(DEDLOC_ERR_INVALID_ARG, "step must be >= 1");
+    lp.lr = cfg->lr;
+    lp.beta1 = cfg->beta1;
+    lp.beta2 = cfg->beta2;
+    lp.omb1 = 1.0f - cfg->beta1;
+    lp.omb2 = 1.0f - cfg->beta2;
+    lp.c1 = 1.0f;
+    lp.c2 = 1.0f;
+    if (cfg->bias_correction) {
+        lp.c1 = (float)(1.0 - pow((double)cfg->beta1, (double)cfg->step));
+        lp.c2 = (float)(1.0 - pow((double)cfg->beta2, (double)cfg->step));
+    }
+    lp.eps = cfg->eps;
+    lp.wd = cfg->weight_decay;
+    lp.unit_trust = cfg->force_unit_trust ? 1 : 0;
+    return DEDLOC_OK;
+}
+
+int check_state(float *x, float *m, float *v, void *ws, size_t ws_bytes, const Plan &pl) {
+    if (!x || !m || !v) return fail(DEDLOC_ERR_INVALID_ARG, "x, m and v must not be NULL");
+    if (!aligned(x, 16) || !aligned(m, 16) || !aligned(v, 16))
+        return fail(DEDLOC_ERR_ALIGN, "x, m and v must be 16-byte aligned");
+    if (!ws || ws_bytes < pl.ws_total)
+        return fail(DEDLOC_ERR_WORKSPACE, "workspace of %zu bytes needed (got %zu)", pl.ws_total,
+                    ws ? ws_bytes : (size_t)0);
+    if (!aligned(ws, 256)) return fail(DEDLOC_ERR_ALIGN, "workspace must be 256-byte aligned");
+    return DEDLOC_OK;
+}
+
+// Pass A over every chunk, then pass B over every chunk.
+int run_lamb(int src, const Plan &pl, const PeerTable *pt, const GradArgs &ga, const LambParams &lp,
+             float *x, float *m, float *v, void *ws, float *trust_out, hipStream_t s) {
+    const LambWs w = carve(pl, ws);
+    for (size_t c = 0; c < pl.chunks.size(); c++) {
+        // a chunk of empty tensors still runs one block to publish r = 1
+        const uint32_t grid = pl.chunk_tiles[c] ? pl.chunk_tiles[c] : 1;
+        hipError_t e = timed(K_LAMB_A_F32 + src, s, [&] { return launch_lamb_a(src, pl.chunks[c], grid, pt, ga, lp, x, m, v, w, trust_out, s); });
+        if (e != hipSuccess) return hip_fail(e, "LAMB pass A launch");
+    }
+    for (size_t c = 0; c < pl.chunks.size(); c++) {
+        if (pl.chunk_tiles[c] == 0) continue;
+        hipError_t e = timed(K_LAMB_B, s, [&] { return launch_lamb_b(pl.chunks[c], pl.chunk_tiles[c], lp, x, m, v, w, s); });
+        if (e != hipSuccess) return hip_fail(e, "LAMB pass B launch");
+    }
+    return DEDLOC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dedloc_version(void) { return 100; }
+
+const char *dedloc_last_error(void) { return g_err.c_str(); }
+
+size_t dedloc_encoded_bytes(int32_t codec, uint32_t block, uint64_t n, uint64_t *n_scales) {
+    if (n_scales) *n_scales = 0;
+    if (codec == DEDLOC_CODEC_FP16) return (size_t)n * 2;
+    if (codec == DEDLOC_CODEC_I8 && block > 0) {
+        if (n_scales) *n_scales = (n + block - 1) / block;
+        return (size_t)n;
+    }
+    if (codec == DEDLOC_CODEC_F32) return (size_t)n * 4;
+    return 0;
+}
+
+int dedloc_partition(uint64_t P, uint32_t n_shards, const uint64_t *weights, uint32_t align,
+                     uint64_t *bounds) {
+    if (!bounds) return fail(DEDLOC_ERR_INVALID_ARG, "bounds must not be NULL");
+    if (n_shards == 0 || align == 0) return fail(DEDLOC_ERR_INVALID_ARG, "n_shards and align must be > 0");
+    unsigned __int128 total = 0;
+    for (uint32_t k = 0; k < n_shards; k++) total += weights ? weights[k] : 1;
+    if (total == 0) return fail(DEDLOC_ERR_INVALID_ARG, "all shard weights are zero");
+    const unsigned __int128 denom = total * align;
+    unsigned __int128 c = 0;
+    bounds[0] = 0;
+    for (uint32_t k = 1; k < n_shards; k++) {
+        c += weights ? weights[k - 1] : 1;
+        bounds[k] = (uint64_t)(((unsigned __int128)P * c / denom) * align);
+    }
+    bounds[n_shards] = P;
+    return DEDLOC_OK;
+}
+
+int dedloc_weights(const uint32_t *counts, uint32_t n, float *w) {
+    if (!counts || !w || n == 0) return fail(DEDLOC_ERR_INVALID_ARG, "counts/w must be non-NULL, n > 0");
+    return compute_weights(counts, n, w);
+}
+
+int dedloc_encode(const float *x, uint64_t n, int32_t codec, uint32_t block, void *codes,
+                  float *scales, void *stream) {
+    int rc = check_codec(codec, block, false);
+    if (rc) return rc;
+    if (n == 0) return DEDLOC_OK;
+    if (!x || !codes) return fail(DEDLOC_ERR_INVALID_ARG, "x and codes must not be NULL");
+    if (!aligned(x, 16) || !aligned(codes, 16)) return fail(DEDLOC_ERR_ALIGN, "x and codes must be 16-byte aligned");
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e;
+    if (codec == DEDLOC_CODEC_FP16) {
+        e = timed(K_ENCODE_FP16, s, [&] { return launch_encode_fp16(x, n, (uint16_t *)codes, s); });
+    } else {
+        if (!scales) return fail(DEDLOC_ERR_INVALID_ARG, "int8 encode needs scales");
+        if (!aligned(scales, 4)) return fail(DEDLOC_ERR_ALIGN, "scales must be 4-byte aligned");
+        e = timed(K_ENCODE_I8, s, [&] { return launch_encode_i8(x, n, (int8_t *)codes, scales, s); });
+    }
+    return e == hipSuccess ? DEDLOC_OK : hip_fail(e, "encode launch");
+}
+
+int dedloc_decode(const void *codes, const float *scales, uint64_t n, int32_t codec, uint32_t block,
+                  float *out, void *stream) {
+    int rc = check_codec(codec, block, false);
+    if (rc) return rc;
+    if (n == 0) return DEDLOC_OK;
+    if (!codes || !out) return fail(DEDLOC_ERR_INVALID_ARG, "codes and out must not be NULL");
+    if (!aligned(out, 16) || !aligned(codes, 16)) return fail(DEDLOC_ERR_ALIGN, "codes and out must be 16-byte aligned");
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e;
+    if (codec == DEDLOC_CODEC_FP16) {
+        e = timed(K_DECODE_FP16, s, [&] { return launch_decode_fp16((const uint16_t *)codes, n, out, s); });
+    } else {
+        if (!scales) return fail(DEDLOC_ERR_INVALID_ARG, "int8 decode needs scales");
+        if (!aligned(scales, 4)) return fail(DEDLOC_ERR_ALIGN, "scales must be 4-byte aligned");
+        e = timed(K_DECODE_I8, s, [&] { return launch_decode_i8((const int8_t *)codes, scales, n, out, s); });
+    }
+    return e == hipSuccess ? DEDLOC_OK : hip_fail(e, "decode launch");
+}
+
+int dedloc_reduce_shard(const void *const *peer_codes, const float *const *peer_scales,
+                        const uint32_t *counts, uint32_t n_peers, uint64_t shard_len, int32_t codec,
+                        uint32_t block, void *out_codes, float *out_scales, float *out_mean,
+                        void *stream) {
+    int rc = check_codec(codec, block, false);
+    if (rc) return rc;
+    PeerTable pt;
+    rc = build_peers(peer_codes, peer_scales, counts, n_peers, codec, pt, shard_len > 0);
+    if (rc) return rc;
+    if (shard_len == 0) return DEDLOC_OK;
+    if (!out_codes || !aligned(out_codes, 16)) return fail(DEDLOC_ERR_ALIGN, "out_codes must be non-NULL and 16-byte aligned");
+    if (out_mean && !aligned(out_mean, 16)) return fail(DEDLOC_ERR_ALIGN, "out_mean must be 16-byte aligned");
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e;
+    if (codec == DEDLOC_CODEC_FP16) {
+        e = timed(K_REDUCE_FP16, s, [&] { return launch_reduce_fp16(pt, shard_len, (uint16_t *)out_codes, out_mean, s); });
+    } else {
+        if (!out_scales || !aligned(out_scales, 4)) return fail(DEDLOC_ERR_INVALID_ARG, "int8 reduce needs aligned out_scales");
+        e = timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(pt, shard_len, (int8_t *)out_codes, out_scales, out_mean, s); });
+    }
+    return e == hipSuccess ? DEDLOC_OK : hip_fail(e, "reduce launch");
+}
+
+size_t dedloc_lamb_workspace_bytes(uint64_t P, const uint64_t *offsets, uint32_t n_tensors) {
+    if (check_tensors(P, offsets, n_tensors)) return 0;
+    Plan pl;
+    make_plan(P, offsets, nullptr, n_tensors, pl);
+    return pl.ws_total;
+}
+
+int dedloc_workspace_clear(void *ws, size_t ws_bytes, void *stream) {
+    if (!ws || !aligned(ws, 4)) return fail(DEDLOC_ERR_INVALID_ARG, "workspace must be non-NULL and 4-byte aligned");
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = timed(K_FILL, s, [&] { return launch_fill_zero(ws, ws_bytes, s); });
+    return e == hipSuccess ? DEDLOC_OK : hip_fail(e, "workspace clear launch");
+}
+
+int dedloc_lamb_step(float *x, float *m, float *v, const void *grad, const float *grad_scales,
+                     int32_t grad_codec, uint32_t block, uint64_t P, const uint64_t *offsets,
+                     const uint8_t *flags, uint32_t n_tensors, const dedloc_lamb_cfg *cfg,
+                     float *trust_out, void *ws, size_t ws_bytes, void *stream) {
+    int rc = check_codec(grad_codec, block, true);
+    if (rc) return rc;
+    rc = check_tensors(P, offsets, n_tensors);
+    if (rc) return rc;
+    if (!flags) return fail(DEDLOC_ERR_INVALID_ARG, "flags must not be NULL");
+    LambParams lp;
+    rc = make_params(cfg, lp);
+    if (rc) return rc;
+    Plan pl;
+    make_plan(P, offsets, flags, n_tensors, pl);
+    rc = check_state(x, m, v, ws, ws_bytes, pl);
+    if (rc) return rc;
+    if (!grad || !aligned(grad, 16)) return fail(DEDLOC_ERR_ALIGN, "grad must be non-NULL and 16-byte aligned");
+    if (grad_codec == DEDLOC_CODEC_I8 && (!grad_scales || !aligned(grad_scales, 4)))
+        return fail(DEDLOC_ERR_INVALID_ARG, "int8 gradient needs aligned grad_scales");
+    GradArgs ga = {grad, grad_scales, nullptr, nullptr};
+    const int src = grad_codec == DEDLOC_CODEC_F32 ? kSrcF32 : grad_codec == DEDLOC_CODEC_FP16 ? kSrcFP16 : kSrcI8;
+    return run_lamb(src, pl, nullptr, ga, lp, x, m, v, ws, trust_out, (hipStream_t)stream);
+}
+
+int dedloc_round(const void *const *peer_codes, const float *const *peer_scales, const uint32_t *counts,
+                 uint32_t n_peers, const uint64_t *bounds, uint32_t n_shards, int32_t codec, uint32_t block,
+                 void *out_codes, float *out_scales, float *x, float *m, float *v, uint64_t P,
+                 const uint64_t *offsets, const uint8_t *flags, uint32_t n_tensors,
+                 const dedloc_lamb_cfg *cfg, float *trust_out, float *out_mean, void *ws, size_t ws_bytes,
+                 void *stream) {
+    int rc = check_codec(codec, block, false);
+    if (rc) return rc;
+    PeerTable pt;
+    rc = build_peers(peer_codes, peer_scales, counts, n_peers, codec, pt);
+    if (rc) return rc;
+    if (!bounds || n_shards == 0) return fail(DEDLOC_ERR_INVALID_ARG, "bounds must list n_shards >= 1 shards");
+    if (bounds[0] != 0 || bounds[n_shards] != P) return fail(DEDLOC_ERR_INVALID_ARG, "shard bounds must tile [0, P)");
+    for (uint32_t k = 0; k < n_shards; k++) {
+        if (bounds[k + 1] < bounds[k]) return fail(DEDLOC_ERR_INVALID_ARG, "shard bounds decrease at %u", k);
+        if (codec == DEDLOC_CODEC_I8 && k > 0 && bounds[k] % block)
+            return fail(DEDLOC_ERR_INVALID_ARG, "int8 shard bound %u is not a multiple of the block", k);
+    }
+    rc = check_tensors(P, offsets, n_tensors);
+    if (rc) return rc;
+    if (!flags) return fail(DEDLOC_ERR_INVALID_ARG, "flags must not be NULL");
+    LambParams lp;
+    rc = make_params(cfg, lp);
+    if (rc) return rc;
+    Plan pl;
+    make_plan(P, offsets, flags, n_tensors, pl);
+    rc = check_state(x, m, v, ws, ws_bytes, pl);
+    if (rc) return rc;
+    if (!out_codes || !aligned(out_codes, 16)) return fail(DEDLOC_ERR_ALIGN, "out_codes must be non-NULL and 16-byte aligned");
+    if (out_mean && !aligned(out_mean, 16)) return fail(DEDLOC_ERR_ALIGN, "out_mean must be 16-byte aligned");
+    hipStream_t s = (hipStream_t)stream;
+    if (codec == DEDLOC_CODEC_FP16) {
+        // Elementwise codec: every shard's average is the same function of
+        // the element index, so the fused pass covers all shards at once.
+        GradArgs ga = {nullptr, nullptr, (uint16_t *)out_codes, out_mean};
+        return run_lamb(kSrcPeersFP16, pl, &pt, ga, lp, x, m, v, ws, trust_out, s);
+    }
+    if (!out_scales || !aligned(out_scales, 4)) return fail(DEDLOC_ERR_INVALID_ARG, "int8 round needs aligned out_scales");
+    // int8: interior shard bounds sit on block boundaries, so every shard's
+    // blocks are the vector's blocks and one pass reduces all shards.
+    hipError_t e = timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(pt, P, (int8_t *)out_codes, out_scales, out_mean, s); });
+    if (e != hipSuccess) return hip_fail(e, "reduce launch");
+    GradArgs ga = {out_codes, out_scales, nullptr, nullptr};
+    return run_lamb(kSrcI8, pl, nullptr, ga, lp, x, m, v, ws, trust_out, s);
+}
+
+int dedloc_profile_begin(uint32_t max_launches) {
+    std::lock_guard<std::mutex> lk(g_prof.mu);
+    g_prof.on = true;
+    g_prof.cap = max_launches;
+    g_prof.used = 0;
+    g_prof.kind.clear();
+    return DEDLOC_OK;
+}
+
+int dedloc_profile_end(uint32_t n_kinds, double *total_ms, uint64_t *launches) {
+    std::lock_guard<std::mutex> lk(g_prof.mu);
+    if (!g_prof.on) return fail(DEDLOC_ERR_INVALID_ARG, "profiling was not started");
+    g_prof.on = false;
+    for (uint32_t k = 0; k < n_kinds; k++) {
+        if (total_ms) total_ms[k] = 0.0;
+        if (launches) launches[k] = 0;
+    }
+    for (size_t i = 0; i < g_prof.used; i++) {
+        hipError_t r = hipEventSynchronize(g_prof.ev[2 * i + 1]);
+        if (r != hipSuccess) return hip_fail(r, "profile event wait");
+        float ms = 0.0f;
+        r = hipEventElapsedTime(&ms, g_prof.ev[2 * i], g_prof.ev[2 * i + 1]);
+        if (r != hipSuccess) return hip_fail(r, "profile event time");
+        const int k = g_prof.kind[i];
+        if ((uint32_t)k < n_kinds) {
+            if (total_ms) total_ms[k] += ms;
+            if (launches) launches[k] += 1;
+        }
+    }
+    g_prof.used = 0;
+    return DEDLOC_OK;
+}
+
+int dedloc_kernel_kinds(void) { return K_COUNT; }
+
+const char *dedloc_kernel_name(int kind) {
+    return (kind >= 0 && kind < K_COUNT) ? kKindNames[kind] : "";
+}
+
+}  // extern "C"

@@ -1,0 +1,568 @@
+// gfx950 kernels of libdedloc: wire codecs, the weighted shard average and
+// the two LAMB passes.
+//
+// Every kernel streams HBM in 16-byte vectors per lane; nothing here is a
+// dense contraction, so there is no MFMA.  Compiled with -ffp-contract=off:
+// every fused multiply-add is an explicit fmaf, every other operation rounds
+// once, fp32 division and square root are correctly rounded (the HIP
+// defaults), so the results are fixed by the definitions in dedloc.h.
+#include "dedloc_internal.h"
+
+namespace dedloc {
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- helpers
+
+__device__ __forceinline__ float h2f(unsigned bits) {
+    return (float)__builtin_bit_cast(_Float16, (uint16_t)bits);
+}
+__device__ __forceinline__ unsigned f2h(float f) {
+    // IEEE round to nearest even, gradual underflow, overflow to infinity
+    return __builtin_bit_cast(uint16_t, (_Float16)f);
+}
+
+__device__ __forceinline__ void unpack_fp16x8(u32x4 c, float *o) {
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        o[2 * i] = h2f(c[i] & 0xffffu);
+        o[2 * i + 1] = h2f(c[i] >> 16);
+    }
+}
+__device__ __forceinline__ u32x4 pack_fp16x8(const float *a) {
+    u32x4 c;
+#pragma unroll
+    for (int i = 0; i < 4; i++) c[i] = f2h(a[2 * i]) | (f2h(a[2 * i + 1]) << 16);
+    return c;
+}
+
+__device__ __forceinline__ float sbyte(unsigned word, int j) {
+    return (float)(int)(int8_t)(word >> (8 * j));
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+// Sum of two doubles over the 256-thread block in a fixed tree; thread 0
+// gets the result.
+__device__ __forceinline__ void block_sum2(double &a, double &b) {
+    __shared__ double red[2][kWG / 64];
+    a = wave_sum(a);
+    b = wave_sum(b);
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    if (lane == 0) {
+        red[0][wave] = a;
+        red[1][wave] = b;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        a = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+        b = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+    }
+    __syncthreads();
+}
+
+// Encode one int8 block held by a wave: 16 values per lane, `nvalid` of them
+// real (the rest are zero).  Returns the codes packed in a u32x4 and the
+// block scale (same on every lane).
+__device__ __forceinline__ u32x4 encode_i8_wave(const float *val, float &scale) {
+    float a = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kI8PerLane; j++) a = fmaxf(a, fabsf(val[j]));
+    a = wave_max(a);
+    const float s = a / 127.0f;
+    scale = (a == 0.0f) ? 0.0f : s;
+    u32x4 c = {0u, 0u, 0u, 0u};
+    if (a != 0.0f) {
+#pragma unroll
+        for (int j = 0; j < kI8PerLane; j++) {
+            float q = rintf(val[j] / s);
+            q = fminf(fmaxf(q, -127.0f), 127.0f);
+            c[j >> 2] |= ((unsigned)(int)q & 0xffu) << (8 * (j & 3));
+        }
+    }
+    return c;
+}
+
+// -------------------------------------------------------------- fp16 codec
+
+__global__ __launch_bounds__(kWG) void encode_fp16_kernel(const float *__restrict__ x, uint64_t n,
+                                                          uint16_t *__restrict__ codes) {
+    const uint64_t e0 = ((uint64_t)blockIdx.x * kWG + threadIdx.x) * kVec;
+    if (e0 + kVec <= n) {
+        const f32x4 a = *(const f32x4 *)(x + e0), b = *(const f32x4 *)(x + e0 + 4);
+        float v[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+        *(u32x4 *)(codes + e0) = pack_fp16x8(v);
+    } else {
+        for (uint64_t e = e0; e < n; e++) codes[e] = (uint16_t)f2h(x[e]);
+    }
+}
+
+__global__ __launch_bounds__(kWG) void decode_fp16_kernel(const uint16_t *__restrict__ codes, uint64_t n,
+                                                          float *__restrict__ out) {
+    const uint64_t e0 = ((uint64_t)blockIdx.x * kWG + threadIdx.x) * kVec;
+    if (e0 + kVec <= n) {
+        float v[8];
+        unpack_fp16x8(*(const u32x4 *)(codes + e0), v);
+        *(f32x4 *)(out + e0) = f32x4{v[0], v[1], v[2], v[3]};
+        *(f32x4 *)(out + e0 + 4) = f32x4{v[4], v[5], v[6], v[7]};
+    } else {
+        for (uint64_t e = e0; e < n; e++) out[e] = h2f(codes[e]);
+    }
+}
+
+// -------------------------------------------------------------- int8 codec
+// One wave per 1024-element block, 16 elements per lane.
+
+__global__ __launch_bounds__(kWG) void encode_i8_kernel(const float *__restrict__ x, uint64_t n,
+                                                        int8_t *__restrict__ codes,
+                                                        float *__restrict__ scales) {
+    const uint64_t blk = (uint64_t)blockIdx.x * (kWG / 64) + (threadIdx.x >> 6);
+    const uint64_t e0 = blk * kI8Block + (threadIdx.x & 63) * kI8PerLane;
+    if (blk * kI8Block >= n) return;  // whole wave past the end
+    float val[kI8PerLane];
+    if (e0 + kI8PerLane <= n) {
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+            const f32x4 a = *(const f32x4 *)(x + e0 + 4 * q);
+            val[4 * q] = a[0]; val[4 * q + 1] = a[1]; val[4 * q + 2] = a[2]; val[4 * q + 3] = a[3];
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < kI8PerLane; j++) val[j] = (e0 + j < n) ? x[e0 + j] : 0.0f;
+    }
+    float s;
+    const u32x4 c = encode_i8_wave(val, s);
+    if (e0 + kI8PerLane <= n) {
+        *(u32x4 *)(codes + e0) = c;
+    } else {
+        for (int j = 0; j < kI8PerLane; j++)
+            if (e0 + j < n) codes[e0 + j] = (int8_t)(c[j >> 2] >> (8 * (j & 3)));
+    }
+    if ((threadIdx.x & 63) == 0) scales[blk] = s;
+}
+
+__global__ __launch_bounds__(kWG) void decode_i8_kernel(const int8_t *__restrict__ codes,
+                                                        const float *__restrict__ scales, uint64_t n,
+                                                        float *__restrict__ out) {
+    const uint64_t e0 = ((uint64_t)blockIdx.x * kWG + threadIdx.x) * kI8PerLane;
+    if (e0 >= n) return;
+    const float s = scales[e0 / kI8Block];
+    if (e0 + kI8PerLane <= n) {
+        const u32x4 c = *(const u32x4 *)(codes + e0);
+#pragma unroll
+        for (int q = 0; q < 4; q++)
+            *(f32x4 *)(out + e0 + 4 * q) = f32x4{sbyte(c[q], 0) * s, sbyte(c[q], 1) * s,
+                                                 sbyte(c[q], 2) * s, sbyte(c[q], 3) * s};
+    } else {
+        for (uint64_t e = e0; e < n; e++) out[e] = (float)codes[e] * s;
+    }
+}
+
+// ------------------------------------------------------------- the reducer
+// mean[e] = sum over active peers (ascending) of w_p * dec_p[e], one fma per
+// peer starting from +0.
+
+// Eight consecutive fp16 elements starting at e0 (all in range).
+__device__ __forceinline__ void reduce_fp16x8(const PeerTable &pt, uint64_t e0, float *acc) {
+#pragma unroll
+    for (int i = 0; i < 8; i++) acc[i] = 0.0f;
+    constexpr int B = 8;  // peer loads kept in flight per lane
+    for (uint32_t p0 = 0; p0 < pt.n; p0 += B) {
+        u32x4 c[B];
+#pragma unroll
+        for (int j = 0; j < B; j++)
+            if (p0 + j < pt.n) c[j] = *(const u32x4 *)((const uint16_t *)pt.codes[p0 + j] + e0);
+#pragma unroll
+        for (int j = 0; j < B; j++) {
+            if (p0 + j < pt.n) {
+                const float w = pt.w[p0 + j];
+                float d[8];
+                unpack_fp16x8(c[j], d);
+#pragma unroll
+                for (int i = 0; i < 8; i++) acc[i] = fmaf(w, d[i], acc[i]);
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ float reduce_fp16_one(const PeerTable &pt, uint64_t e) {
+    float acc = 0.0f;
+    for (uint32_t p = 0; p < pt.n; p++)
+        acc = fmaf(pt.w[p], h2f(((const uint16_t *)pt.codes[p])[e]), acc);
+    return acc;
+}
+
+__global__ __launch_bounds__(kWG) void reduce_fp16_kernel(const PeerTable pt, uint64_t len,
+                                                          uint16_t *__restrict__ out,
+                                                          float *__restrict__ mean) {
+    const uint64_t e0 = ((uint64_t)blockIdx.x * kWG + threadIdx.x) * kVec;
+    if (e0 + kVec <= len) {
+        float acc[8];
+        reduce_fp16x8(pt, e0, acc);
+        *(u32x4 *)(out + e0) = pack_fp16x8(acc);
+        if (mean) {
+            *(f32x4 *)(mean + e0) = f32x4{acc[0], acc[1], acc[2], acc[3]};
+            *(f32x4 *)(mean + e0 + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
+        }
+    } else {
+        for (uint64_t e = e0; e < len; e++) {
+            const float a = reduce_fp16_one(pt, e);
+            out[e] = (uint16_t)f2h(a);
+            if (mean) mean[e] = a;
+        }
+    }
+}
+
+// One wave per 1024-element block; lane holds 16 elements.
+__global__ __launch_bounds__(kWG) void reduce_i8_kernel(const PeerTable pt, uint64_t len,
+                                                        int8_t *__restrict__ out,
+                                                        float *__restrict__ out_scales,
+                                                        float *__restrict__ mean) {
+    const uint64_t blk = (uint64_t)blockIdx.x * (kWG / 64) +
+                         (uint64_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (blk * kI8Block >= len) return;  // whole wave past the end
+    const uint64_t e0 = blk * kI8Block + (threadIdx.x & 63) * kI8PerLane;
+    const bool full = e0 + kI8PerLane <= len;
+    float acc[kI8PerLane];
+#pragma unroll
+    for (int j = 0; j < kI8PerLane; j++) acc[j] = 0.0f;
+    constexpr int B = 4;
+    for (uint32_t p0 = 0; p0 < pt.n; p0 += B) {
+        u32x4 c[B];
+        float s[B];
+#pragma unroll
+        for (int j = 0; j < B; j++) {
+            if (p0 + j < pt.n) {
+                const int8_t *src = (const int8_t *)pt.codes[p0 + j];
+                s[j] = pt.scales[p0 + j][blk];
+                if (full) {
+                    c[j] = *(const u32x4 *)(src + e0);
+                } else {
+                    c[j] = u32x4{0u, 0u, 0u, 0u};
+                    for (int k = 0; k < kI8PerLane; k++)
+                        if (e0 + k < len) c[j][k >> 2] |= ((unsigned)(uint8_t)src[e0 + k]) << (8 * (k & 3));
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < B; j++) {
+            if (p0 + j < pt.n) {
+                const float w = pt.w[p0 + j];
+#pragma unroll
+                for (int k = 0; k < kI8PerLane; k++) {
+                    const float d = sbyte(c[j][k >> 2], k & 3) * s[j];
+                    acc[k] = fmaf(w, d, acc[k]);
+                }
+            }
+        }
+    }
+    float s;
+    const u32x4 c = encode_i8_wave(acc, s);  // out-of-range lanes hold 0
+    if (full) {
+        *(u32x4 *)(out + e0) = c;
+        if (mean) {
+#pragma unroll
+            for (int q = 0; q < 4; q++)
+                *(f32x4 *)(mean + e0 + 4 * q) = f32x4{acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
+        }
+    } else {
+        for (int k = 0; k < kI8PerLane; k++) {
+            if (e0 + k < len) {
+                out[e0 + k] = (int8_t)(c[k >> 2] >> (8 * (k & 3)));
+                if (mean) mean[e0 + k] = acc[k];
+            }
+        }
+    }
+    if ((threadIdx.x & 63) == 0) out_scales[blk] = s;
+}
+
+// ------------------------------------------------------------------- LAMB
+
+__device__ __forceinline__ float lamb_dir(float mn, float vn, float x, float lam,
+                                          const LambParams &lp) {
+    const float mh = mn / lp.c1;
+    const float vh = vn / lp.c2;
+    return mh / (sqrtf(vh) + lp.eps) + lam * x;
+}
+
+// Tensor of launch block b: the largest k with tile_begin[k] <= b (empty
+// tensors own no blocks and are skipped).  All values are wave-uniform.
+__device__ __forceinline__ uint32_t chunk_tensor(const Chunk &ch, uint32_t b) {
+    uint32_t lo = 0, hi = ch.nt;
+    while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (ch.tile_begin[mid] <= b) lo = mid;
+        else hi = mid;
+    }
+    return lo;
+}
+
+// Gradient of the elements [e0, e0+cnt), cnt <= 8, for source SRC.
+template <int SRC>
+__device__ __forceinline__ void load_grad(const GradArgs &ga, const PeerTable &pt, uint64_t e0,
+                                          int cnt, float *g) {
+    if (cnt == kVec) {
+        if (SRC == kSrcF32) {
+            const f32x4 a = *(const f32x4 *)((const float *)ga.grad + e0);
+            const f32x4 b = *(const f32x4 *)((const float *)ga.grad + e0 + 4);
+            g[0] = a[0]; g[1] = a[1]; g[2] = a[2]; g[3] = a[3];
+            g[4] = b[0]; g[5] = b[1]; g[6] = b[2]; g[7] = b[3];
+        } else if (SRC == kSrcFP16) {
+            unpack_fp16x8(*(const u32x4 *)((const uint16_t *)ga.grad + e0), g);
+        } else if (SRC == kSrcI8) {
+            const u32x2 c = *(const u32x2 *)((const int8_t *)ga.grad + e0);
+            const float s = ga.scales[e0 / kI8Block];
+#pragma unroll
+            for (int j = 0; j < 8; j++) g[j] = sbyte(c[j >> 2], j & 3) * s;
+        } else {
+            float acc[8];
+            reduce_fp16x8(pt, e0, acc);
+            const u32x4 c = pack_fp16x8(acc);
+            *(u32x4 *)(ga.out_codes + e0) = c;
+            if (ga.out_mean) {
+                *(f32x4 *)(ga.out_mean + e0) = f32x4{acc[0], acc[1], acc[2], acc[3]};
+                *(f32x4 *)(ga.out_mean + e0 + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
+            }
+            unpack_fp16x8(c, g);
+        }
+    } else {
+        for (int j = 0; j < kVec; j++) {
+            if (j >= cnt) {
+                g[j] = 0.0f;
+                continue;
+            }
+            const uint64_t e = e0 + j;
+            if (SRC == kSrcF32) {
+                g[j] = ((const float *)ga.grad)[e];
+            } else if (SRC == kSrcFP16) {
+                g[j] = h2f(((const uint16_t *)ga.grad)[e]);
+            } else if (SRC == kSrcI8) {
+                g[j] = (float)((const int8_t *)ga.grad)[e] * ga.scales[e / kI8Block];
+            } else {
+                const float a = reduce_fp16_one(pt, e);
+                const unsigned c = f2h(a);
+                ga.out_codes[e] = (uint16_t)c;
+                if (ga.out_mean) ga.out_mean[e] = a;
+                g[j] = h2f(c);
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ void load8(const float *p, uint64_t e0, int cnt, float *o) {
+    if (cnt == kVec) {
+        const f32x4 a = *(const f32x4 *)(p + e0), b = *(const f32x4 *)(p + e0 + 4);
+        o[0] = a[0]; o[1] = a[1]; o[2] = a[2]; o[3] = a[3];
+        o[4] = b[0]; o[5] = b[1]; o[6] = b[2]; o[7] = b[3];
+    } else {
+        for (int j = 0; j < kVec; j++) o[j] = j < cnt ? p[e0 + j] : 0.0f;
+    }
+}
+
+__device__ __forceinline__ void store8(float *p, uint64_t e0, int cnt, const float *o) {
+    if (cnt == kVec) {
+        *(f32x4 *)(p + e0) = f32x4{o[0], o[1], o[2], o[3]};
+        *(f32x4 *)(p + e0 + 4) = f32x4{o[4], o[5], o[6], o[7]};
+    } else {
+        for (int j = 0; j < cnt; j++) p[e0 + j] = o[j];
+    }
+}
+
+// Pass A: gradient (optionally the fused average), new moments, and the
+// per-tile sums of x^2 and u^2.  The last tile of each tensor to finish sums
+// the tensor's tile partials in tile order and publishes its trust ratio.
+template <int SRC>
+__global__ __launch_bounds__(kWG) void lamb_a_kernel(const Chunk ch, const PeerTable pt,
+                                                     const GradArgs ga, const LambParams lp,
+                                                     const float *__restrict__ x,
+                                                     float *__restrict__ m, float *__restrict__ v,
+                                                     LambWs ws, float *__restrict__ trust_out) {
+    __shared__ int s_last;
+    const uint32_t b = blockIdx.x;
+    const uint32_t k = chunk_tensor(ch, b);
+    const uint64_t t_lo = ch.off[k], t_hi = ch.off[k + 1];
+    const uint32_t tile = b - ch.tile_begin[k];
+    const uint64_t e0 = t_lo + (uint64_t)tile * kTile + (uint64_t)threadIdx.x * kVec;
+    const float lam = (ch.flags[k] & 1u) ? lp.wd : 0.0f;
+
+    if (b == 0 && threadIdx.x < ch.nt && ch.off[threadIdx.x] == ch.off[threadIdx.x + 1]) {
+        // an empty tensor has both norms 0: its ratio is 1
+        ws.trust[ch.t0 + threadIdx.x] = 1.0f;
+        if (trust_out) trust_out[ch.t0 + threadIdx.x] = 1.0f;
+    }
+    if (b >= ch.tile_begin[ch.nt]) return;  // the lone block of a chunk without tiles
+
+    double sx = 0.0, su = 0.0;
+    if (e0 < t_hi) {
+        const int cnt = (int)(t_hi - e0 < (uint64_t)kVec ? t_hi - e0 : (uint64_t)kVec);
+        float g[8], xv[8], mv[8], vv[8];
+        load_grad<SRC>(ga, pt, e0, cnt, g);
+        load8(x, e0, cnt, xv);
+        load8(m, e0, cnt, mv);
+        load8(v, e0, cnt, vv);
+#pragma unroll
+        for (int j = 0; j < 8; j++) {
+            const float mn = fmaf(lp.beta1, mv[j], lp.omb1 * g[j]);
+            const float vn = fmaf(lp.beta2, vv[j], lp.omb2 * (g[j] * g[j]));
+            const float u = lamb_dir(mn, vn, xv[j], lam, lp);
+            mv[j] = mn;
+            vv[j] = vn;
+            if (j < cnt) {
+                sx += (double)xv[j] * (double)xv[j];
+                su += (double)u * (double)u;
+            }
+        }
+        store8(m, e0, cnt, mv);
+        store8(v, e0, cnt, vv);
+    }
+
+    block_sum2(sx, su);
+    const uint32_t ntiles = ch.tile_begin[k + 1] - ch.tile_begin[k];
+    const uint32_t first_slot = ch.tile_base + ch.tile_begin[k];
+    if (threadIdx.x == 0) {
+        __hip_atomic_store(&ws.partials[2 * (ch.tile_base + b)], sx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&ws.partials[2 * (ch.tile_base + b) + 1], su, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const unsigned prev = __hip_atomic_fetch_add(&ws.counters[ch.t0 + k], 1u, __ATOMIC_ACQ_REL,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+        s_last = (prev == ntiles - 1);
+    }
+    __syncthreads();
+    if (!s_last) return;
+
+    // last tile of tensor k: fixed-order sum of its tiles' partials
+    __atomic_thread_fence(__ATOMIC_ACQUIRE);
+    double ax = 0.0, au = 0.0;
+    for (uint32_t i = threadIdx.x; i < ntiles; i += kWG) {
+        ax += __hip_atomic_load(&ws.partials[2 * (first_slot + i)], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        au += __hip_atomic_load(&ws.partials[2 * (first_slot + i) + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    block_sum2(ax, au);
+    if (threadIdx.x == 0) {
+        const double X = sqrt(ax), U = sqrt(au);
+        float r = 1.0f;
+        if (!lp.unit_trust && (ch.flags[k] & 2u) && X > 0.0 && U > 0.0) r = (float)(X / U);
+        ws.trust[ch.t0 + k] = r;
+        if (trust_out) trust_out[ch.t0 + k] = r;
+        __hip_atomic_store(&ws.counters[ch.t0 + k], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+// Pass B: x' = x - (lr * r_t) * u, with u recomputed from x, m', v' by the
+// same operations as pass A.
+__global__ __launch_bounds__(kWG) void lamb_b_kernel(const Chunk ch, const LambParams lp,
+                                                     float *__restrict__ x,
+                                                     const float *__restrict__ m,
+                                                     const float *__restrict__ v, LambWs ws) {
+    const uint32_t b = blockIdx.x;
+    const uint32_t k = chunk_tensor(ch, b);
+    const uint64_t t_hi = ch.off[k + 1];
+    const uint64_t e0 = ch.off[k] + (uint64_t)(b - ch.tile_begin[k]) * kTile + (uint64_t)threadIdx.x * kVec;
+    if (e0 >= t_hi) return;
+    const int cnt = (int)(t_hi - e0 < (uint64_t)kVec ? t_hi - e0 : (uint64_t)kVec);
+    const float lam = (ch.flags[k] & 1u) ? lp.wd : 0.0f;
+    const float lrr = lp.lr * ws.trust[ch.t0 + k];
+    float xv[8], mv[8], vv[8];
+    load8(x, e0, cnt, xv);
+    load8(m, e0, cnt, mv);
+    load8(v, e0, cnt, vv);
+#pragma unroll
+    for (int j = 0; j < 8; j++) xv[j] = xv[j] - lrr * lamb_dir(mv[j], vv[j], xv[j], lam, lp);
+    store8(x, e0, cnt, xv);
+}
+
+__global__ __launch_bounds__(kWG) void fill_zero_kernel(uint32_t *p, uint64_t n_words) {
+    const uint64_t i = (uint64_t)blockIdx.x * kWG + threadIdx.x;
+    if (i < n_words) p[i] = 0u;
+}
+
+// --------------------------------------------------------------- launchers
+
+static inline unsigned grid_for(uint64_t items, uint64_t per_block) {
+    return (unsigned)((items + per_block - 1) / per_block);
+}
+
+#define DEDLOC_LAUNCH(grid, kernel, ...)                                   \
+    do {                                                                   \
+        const dim3 g_ = (grid);                                            \
+        if (g_.x == 0) return hipSuccess; /* nothing to do */              \
+        hipLaunchKernelGGL(kernel, g_, dim3(kWG), 0, __VA_ARGS__);         \
+        return hipGetLastError();                                          \
+    } while (0)
+
+hipError_t launch_encode_fp16(const float *x, uint64_t n, uint16_t *codes, hipStream_t s) {
+    DEDLOC_LAUNCH(dim3(grid_for(n, kTile)), encode_fp16_kernel, s, x, n, codes);
+}
+
+hipError_t launch_decode_fp16(const uint16_t *codes, uint64_t n, float *out, hipStream_t s) {
+    DEDLOC_LAUNCH(dim3(grid_for(n, kTile)), decode_fp16_kernel, s, codes, n, out);
+}
+
+hipError_t launch_encode_i8(const float *x, uint64_t n, int8_t *codes, float *scales, hipStream_t s) {
+    DEDLOC_LAUNCH(dim3(grid_for(n, (uint64_t)kI8Block * (kWG / 64))), encode_i8_kernel, s, x, n, codes, scales);
+}
+
+hipError_t launch_decode_i8(const int8_t *codes, const float *scales, uint64_t n, float *out,
+                            hipStream_t s) {
+    DEDLOC_LAUNCH(dim3(grid_for(n, (uint64_t)kWG * kI8PerLane)), decode_i8_kernel, s, codes, scales, n, out);
+}
+
+hipError_t launch_reduce_fp16(const PeerTable &pt, uint64_t len, uint16_t *out, float *mean,
+                              hipStream_t s) {
+    DEDLOC_LAUNCH(dim3(grid_for(len, kTile)), reduce_fp16_kernel, s, pt, len, out, mean);
+}
+
+hipError_t launch_reduce_i8(const PeerTable &pt, uint64_t len, int8_t *out, float *out_scales,
+                            float *mean, hipStream_t s) {
+    DEDLOC_LAUNCH(dim3(grid_for(len, (uint64_t)kI8Block * (kWG / 64))), reduce_i8_kernel, s, pt, len, out,
+                  out_scales, mean);
+}
+
+hipError_t launch_lamb_a(int src, const Chunk &ch, uint32_t n_tiles, const PeerTable *pt,
+                         const GradArgs &ga, const LambParams &lp, float *x, float *m, float *v,
+                         const LambWs &ws, float *trust_out, hipStream_t s) {
+    static const PeerTable empty = {};
+    const PeerTable &p = pt ? *pt : empty;
+    const dim3 grid(n_tiles), block(kWG);
+    switch (src) {
+    case kSrcF32:
+        hipLaunchKernelGGL(lamb_a_kernel<kSrcF32>, grid, block, 0, s, ch, p, ga, lp, x, m, v, ws, trust_out);
+        break;
+    case kSrcFP16:
+        hipLaunchKernelGGL(lamb_a_kernel<kSrcFP16>, grid, block, 0, s, ch, p, ga, lp, x, m, v, ws, trust_out);
+        break;
+    case kSrcI8:
+        hipLaunchKernelGGL(lamb_a_kernel<kSrcI8>, grid, block, 0, s, ch, p, ga, lp, x, m, v, ws, trust_out);
+        break;
+    case kSrcPeersFP16:
+        hipLaunchKernelGGL(lamb_a_kernel<kSrcPeersFP16>, grid, block, 0, s, ch, p, ga, lp, x, m, v, ws, trust_out);
+        break;
+    default:
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_lamb_b(const Chunk &ch, uint32_t n_tiles, const LambParams &lp, float *x,
+                         const float *m, const float *v, const LambWs &ws, hipStream_t s) {
+    DEDLOC_LAUNCH(dim3(n_tiles), lamb_b_kernel, s, ch, lp, x, m, v, ws);
+}
+
+hipError_t launch_fill_zero(void *p, size_t bytes, hipStream_t s) {
+    const uint64_t words = bytes / 4;
+    if (words == 0) return hipSuccess;
+    DEDLOC_LAUNCH(dim3(grid_for(words, kWG)), fill_zero_kernel, s, (uint32_t *)p, words);
+}
+
+}  // namespace dedloc

@@ -1,0 +1,302 @@
+"""Thin ctypes binding over libdedloc's C ABI (include/dedloc.h).
+
+Each function has the name of the C entry point it calls and only marshals
+arguments: device tensors become raw pointers, the current torch stream
+becomes the HIP stream, host tables become numpy arrays.  Every step of the
+computation runs in the library's HIP kernels; there is no fallback, and a
+missing or unloadable library raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdedloc.so")
+
+DEDLOC_OK = 0
+DEDLOC_ERR_INVALID_ARG = -1
+DEDLOC_ERR_ALIGN = -2
+DEDLOC_ERR_ZERO_WEIGHT = -3
+DEDLOC_ERR_WORKSPACE = -4
+DEDLOC_ERR_HIP = -5
+
+DEDLOC_CODEC_F32 = 0
+DEDLOC_CODEC_FP16 = 1
+DEDLOC_CODEC_I8 = 2
+DEDLOC_I8_BLOCK = 1024
+DEDLOC_MAX_PEERS = 64
+DEDLOC_TENSOR_DECAY = 1
+DEDLOC_TENSOR_ADAPT = 2
+
+CODECS = {"f32": DEDLOC_CODEC_F32, "fp16": DEDLOC_CODEC_FP16, "i8": DEDLOC_CODEC_I8}
+
+
+class DedlocError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"libdedloc error {code}: {msg}")
+        self.code = code
+
+
+class dedloc_lamb_cfg(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float),
+                ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
+                ("weight_decay", ctypes.c_float), ("step", ctypes.c_uint64),
+                ("bias_correction", ctypes.c_int32),
+                ("force_unit_trust", ctypes.c_int32)]
+
+
+def lamb_cfg(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-6, weight_decay=0.01, step=1,
+             bias_correction=True, force_unit_trust=False) -> dedloc_lamb_cfg:
+    return dedloc_lamb_cfg(lr, beta1, beta2, eps, weight_decay, step,
+                           int(bias_correction), int(force_unit_trust))
+
+
+_lib = None
+
+_SIGS = {
+    "dedloc_version": ([], ctypes.c_int),
+    "dedloc_last_error": ([], ctypes.c_char_p),
+    "dedloc_encoded_bytes": ([ctypes.c_int32, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p], ctypes.c_size_t),
+    "dedloc_partition": ([ctypes.c_uint64, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_uint32, ctypes.c_void_p], ctypes.c_int),
+    "dedloc_weights": ([ctypes.c_void_p, ctypes.c_uint32, ctypes.c_void_p], ctypes.c_int),
+    "dedloc_encode": ([ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int32, ctypes.c_uint32, ctypes.c_void_p,
+                       ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
+    "dedloc_decode": ([ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int32, ctypes.c_uint32,
+                       ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
+    "dedloc_reduce_shard": ([ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint64,
+                             ctypes.c_int32, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                             ctypes.c_void_p], ctypes.c_int),
+    "dedloc_lamb_workspace_bytes": ([ctypes.c_uint64, ctypes.c_void_p, ctypes.c_uint32], ctypes.c_size_t),
+    "dedloc_workspace_clear": ([ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p], ctypes.c_int),
+    "dedloc_lamb_step": ([ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                          ctypes.c_int32, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p, ctypes.c_void_p,
+                          ctypes.c_uint32, ctypes.POINTER(dedloc_lamb_cfg), ctypes.c_void_p, ctypes.c_void_p,
+                          ctypes.c_size_t, ctypes.c_void_p], ctypes.c_int),
+    "dedloc_round": ([ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32, ctypes.c_void_p,
+                      ctypes.c_uint32, ctypes.c_int32, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p,
+                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p,
+                      ctypes.c_void_p, ctypes.c_uint32, ctypes.POINTER(dedloc_lamb_cfg), ctypes.c_void_p,
+                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p], ctypes.c_int),
+    "dedloc_profile_begin": ([ctypes.c_uint32], ctypes.c_int),
+    "dedloc_profile_end": ([ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
+    "dedloc_kernel_kinds": ([], ctypes.c_int),
+    "dedloc_kernel_name": ([ctypes.c_int], ctypes.c_char_p),
+}
+
+EXPORTS = tuple(_SIGS)
+
+
+def load():
+    """Load libdedloc.so (building it first only if it is absent)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            from . import build
+            build.build()
+        lib = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            f = getattr(lib, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = lib
+    return _lib
+
+
+def _check(rc: int):
+    if rc != DEDLOC_OK:
+        raise DedlocError(rc, load().dedloc_last_error().decode())
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, np.ndarray):
+        return t.ctypes.data
+    return t.data_ptr()
+
+
+def _dev(t):
+    if t is not None and not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    return _ptr(t)
+
+
+def _stream(stream=None) -> Optional[int]:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _host(a, dtype) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=dtype))
+
+
+def _ptrs(ts: Sequence) -> ctypes.Array:
+    return (ctypes.c_void_p * len(ts))(*[None if t is None else _dev(t) for t in ts])
+
+
+# ------------------------------------------------------------- host helpers
+
+def dedloc_version() -> int:
+    return load().dedloc_version()
+
+
+def dedloc_encoded_bytes(codec: int, block: int, n: int):
+    ns = ctypes.c_uint64(0)
+    nb = load().dedloc_encoded_bytes(codec, block, n, ctypes.byref(ns))
+    return nb, ns.value
+
+
+def dedloc_partition(P: int, n_shards: int, weights=None, align: int = 64) -> np.ndarray:
+    w = None if weights is None else _host(weights, np.uint64)
+    out = np.zeros(n_shards + 1, dtype=np.uint64)
+    _check(load().dedloc_partition(P, n_shards, _ptr(w), align, _ptr(out)))
+    return out
+
+
+def dedloc_weights(counts) -> np.ndarray:
+    c = _host(counts, np.uint32)
+    w = np.zeros(len(c), dtype=np.float32)
+    _check(load().dedloc_weights(_ptr(c), len(c), _ptr(w)))
+    return w
+
+
+# ------------------------------------------------------------- device calls
+
+def dedloc_encode(x, codec: int, block: int = DEDLOC_I8_BLOCK, codes=None, scales=None, stream=None):
+    import torch
+    n = x.numel()
+    if codes is None:
+        codes = torch.empty(n, dtype=torch.int16 if codec == DEDLOC_CODEC_FP16 else torch.int8, device=x.device)
+    if scales is None and codec == DEDLOC_CODEC_I8:
+        scales = torch.empty((n + block - 1) // block, dtype=torch.float32, device=x.device)
+    _check(load().dedloc_encode(_dev(x), n, codec, block, _dev(codes), _dev(scales), _stream(stream)))
+    return codes, scales
+
+
+def dedloc_decode(codes, scales, n: int, codec: int, block: int = DEDLOC_I8_BLOCK, out=None, stream=None):
+    import torch
+    if out is None:
+        out = torch.empty(n, dtype=torch.float32, device=codes.device)
+    _check(load().dedloc_decode(_dev(codes), _dev(scales), n, codec, block, _dev(out), _stream(stream)))
+    return out
+
+
+def dedloc_reduce_shard(peer_codes: Sequence, counts, shard_len: int, codec: int, peer_scales=None,
+                        block: int = DEDLOC_I8_BLOCK, out_codes=None, out_scales=None, out_mean=None,
+                        stream=None):
+    """Average one shard from the peers' messages (None for zero-count peers)."""
+    import torch
+    dev = next(t.device for t in peer_codes if t is not None)
+    if out_codes is None:
+        out_codes = torch.empty(shard_len, dtype=torch.int16 if codec == DEDLOC_CODEC_FP16 else torch.int8,
+                                device=dev)
+    if out_scales is None and codec == DEDLOC_CODEC_I8:
+        out_scales = torch.empty((shard_len + block - 1) // block, dtype=torch.float32, device=dev)
+    cnt = _host(counts, np.uint32)
+    pc = _ptrs(peer_codes)
+    ps = None if peer_scales is None else _ptrs(peer_scales)
+    _check(load().dedloc_reduce_shard(pc, ps, _ptr(cnt), len(peer_codes), shard_len, codec, block,
+                                      _dev(out_codes), _dev(out_scales), _dev(out_mean), _stream(stream)))
+    return out_codes, out_scales
+
+
+def dedloc_lamb_workspace_bytes(P: int, offsets) -> int:
+    off = _host(offsets, np.uint64)
+    n = load().dedloc_lamb_workspace_bytes(P, _ptr(off), len(off) - 1)
+    if n == 0:
+        raise DedlocError(DEDLOC_ERR_INVALID_ARG, load().dedloc_last_error().decode())
+    return n
+
+
+def dedloc_workspace_clear(ws, stream=None):
+    _check(load().dedloc_workspace_clear(_dev(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def make_workspace(P: int, offsets, device="cuda"):
+    """A zero-filled workspace for dedloc_lamb_step / dedloc_round."""
+    import torch
+    nb = dedloc_lamb_workspace_bytes(P, offsets)
+    ws = torch.empty(nb, dtype=torch.uint8, device=device)
+    dedloc_workspace_clear(ws)
+    return ws
+
+
+def dedloc_lamb_step(x, m, v, grad, offsets, flags, cfg: dedloc_lamb_cfg, grad_codec: int = DEDLOC_CODEC_F32,
+                     grad_scales=None, block: int = DEDLOC_I8_BLOCK, trust_out=None, ws=None, stream=None):
+    off = _host(offsets, np.uint64)
+    fl = _host(flags, np.uint8)
+    P = x.numel()
+    if ws is None:
+        ws = make_workspace(P, off, x.device)
+    _check(load().dedloc_lamb_step(_dev(x), _dev(m), _dev(v), _dev(grad), _dev(grad_scales), grad_codec, block,
+                                   P, _ptr(off), _ptr(fl), len(fl), ctypes.byref(cfg), _dev(trust_out),
+                                   _dev(ws), ws.numel(), _stream(stream)))
+    return ws
+
+
+class RoundCall:
+    """Pre-marshalled arguments of one dedloc_round call: building the
+    pointer arrays once keeps per-call host overhead to the C call itself."""
+
+    def __init__(self, peer_codes, counts, bounds, codec, out_codes, x, m, v, offsets, flags,
+                 cfg: dedloc_lamb_cfg, ws, peer_scales=None, out_scales=None, trust_out=None,
+                 out_mean=None, block: int = DEDLOC_I8_BLOCK):
+        self._keep = (peer_codes, peer_scales, out_codes, out_scales, x, m, v, ws, trust_out, out_mean)
+        self.pc = _ptrs(peer_codes)
+        self.ps = None if peer_scales is None else _ptrs(peer_scales)
+        self.cnt = _host(counts, np.uint32)
+        self.bnd = _host(bounds, np.uint64)
+        self.off = _host(offsets, np.uint64)
+        self.fl = _host(flags, np.uint8)
+        self.cfg = cfg
+        self.args = None
+        self.codec, self.block = codec, block
+        self.out = (_dev(out_codes), _dev(out_scales), _dev(x), _dev(m), _dev(v), x.numel(),
+                    _dev(trust_out), _dev(out_mean), _dev(ws), ws.numel())
+
+    def __call__(self, stream=None):
+        oc, osc, x, m, v, P, tr, om, ws, wsb = self.out
+        _check(load().dedloc_round(self.pc, self.ps, _ptr(self.cnt), len(self.cnt), _ptr(self.bnd),
+                                   len(self.bnd) - 1, self.codec, self.block, oc, osc, x, m, v, P,
+                                   _ptr(self.off), _ptr(self.fl), len(self.fl), ctypes.byref(self.cfg),
+                                   tr, om, ws, wsb, _stream(stream)))
+
+
+def dedloc_round(peer_codes, counts, bounds, codec: int, x, m, v, offsets, flags, cfg: dedloc_lamb_cfg,
+                 peer_scales=None, block: int = DEDLOC_I8_BLOCK, out_codes=None, out_scales=None,
+                 trust_out=None, out_mean=None, ws=None, stream=None):
+    """One averaging round; returns (out_codes, out_scales)."""
+    import torch
+    P = x.numel()
+    if out_codes is None:
+        out_codes = torch.empty(P, dtype=torch.int16 if codec == DEDLOC_CODEC_FP16 else torch.int8, device=x.device)
+    if out_scales is None and codec == DEDLOC_CODEC_I8:
+        out_scales = torch.empty((P + block - 1) // block, dtype=torch.float32, device=x.device)
+    if ws is None:
+        ws = make_workspace(P, offsets, x.device)
+    RoundCall(peer_codes, counts, bounds, codec, out_codes, x, m, v, offsets, flags, cfg, ws, peer_scales,
+              out_scales, trust_out, out_mean, block)(stream)
+    return out_codes, out_scales
+
+
+# ------------------------------------------------------------- profiling
+
+def dedloc_profile_begin(max_launches: int = 1 << 16):
+    _check(load().dedloc_profile_begin(max_launches))
+
+
+def dedloc_profile_end():
+    """{kernel name: (total ms, launches)} for the kernels enqueued since
+    dedloc_profile_begin (waits for them)."""
+    lib = load()
+    n = lib.dedloc_kernel_kinds()
+    ms = np.zeros(n, np.float64)
+    cnt = np.zeros(n, np.uint64)
+    _check(lib.dedloc_profile_end(n, _ptr(ms), _ptr(cnt)))
+    return {lib.dedloc_kernel_name(k).decode(): (float(ms[k]), int(cnt[k])) for k in range(n) if cnt[k]}

