@@ -134,14 +134,14 @@ int dedloc_reduce_shard(const void *const *peer_codes, const float *const *peer_
                         float *out_scales, float *out_mean, void *stream);
 
 /* Workspace for dedloc_lamb_step / dedloc_round with this tensor table
- * (offsets: host, n_tensors+1).  Returns 0 for an invalid table.
- * The workspace must be zero-filled once before its first use (for example
- * with dedloc_workspace_clear); every call leaves it in a reusable state.
- * Calls that share one workspace must not overlap in time. */
+ * (offsets: host, n_tensors+1): two fp64 partial sums per 2048-element tile
+ * and one fp32 trust ratio per tensor.  Returns 0 for an invalid table.
+ * Its contents need no initialisation and carry nothing between calls;
+ * calls that share one workspace must not overlap in time. */
 size_t dedloc_lamb_workspace_bytes(uint64_t P, const uint64_t *offsets, uint32_t n_tensors);
 
-/* Zero-fill a workspace with a kernel (no memset node, so it may be
- * captured into a graph). */
+/* Zero-fill a device buffer (for example a workspace) with a kernel: no
+ * memset node, so the call may be captured into a graph. */
 int dedloc_workspace_clear(void *ws, size_t ws_bytes, void *stream);
 
 /* One LAMB step over a flat parameter buffer (Section 3.1 trains with LAMB;

@@ -39,11 +39,13 @@ bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
 // ------------------------------------------------------------ profiling
 enum Kind {
     K_ENCODE_FP16, K_DECODE_FP16, K_ENCODE_I8, K_DECODE_I8, K_REDUCE_FP16, K_REDUCE_I8,
-    K_LAMB_A_F32, K_LAMB_A_FP16, K_LAMB_A_I8, K_LAMB_A_FUSED_FP16, K_LAMB_B, K_FILL, K_COUNT
+    K_LAMB_A_F32, K_LAMB_A_FP16, K_LAMB_A_I8, K_LAMB_A_FUSED_FP16, K_LAMB_TRUST, K_LAMB_B, K_FILL,
+    K_COUNT
 };
 const char *const kKindNames[K_COUNT] = {
     "encode_fp16", "decode_fp16", "encode_i8", "decode_i8", "reduce_fp16", "reduce_i8",
-    "lamb_a_f32", "lamb_a_fp16", "lamb_a_i8", "lamb_a_fused_fp16", "lamb_b", "fill_zero"};
+    "lamb_a_f32", "lamb_a_fp16", "lamb_a_i8", "lamb_a_fused_fp16", "lamb_trust", "lamb_b",
+    "fill_zero"};
 
 struct Profiler {
     std::mutex mu;
@@ -137,7 +139,7 @@ struct Plan {
     std::vector<Chunk> chunks;
     std::vector<uint32_t> chunk_tiles;
     uint32_t n_tiles = 0;
-    size_t ws_partials = 0, ws_counters = 0, ws_trust = 0, ws_total = 0;
+    size_t ws_partials = 0, ws_trust = 0, ws_total = 0;
 };
 
 int check_tensors(uint64_t P, const uint64_t *off, uint32_t T) {
@@ -179,17 +181,15 @@ void make_plan(uint64_t P, const uint64_t *off, const uint8_t *flags, uint32_t T
     }
     pl.n_tiles = base;
     pl.ws_partials = round_up((size_t)base * 2 * sizeof(double), 256);
-    pl.ws_counters = round_up((size_t)T * sizeof(unsigned), 256);
     pl.ws_trust = round_up((size_t)T * sizeof(float), 256);
-    pl.ws_total = pl.ws_partials + pl.ws_counters + pl.ws_trust;
+    pl.ws_total = pl.ws_partials + pl.ws_trust;
 }
 
 LambWs carve(const Plan &pl, void *ws) {
     char *b = (char *)ws;
     LambWs w;
     w.partials = (double *)b;
-    w.counters = (unsigned *)(b + pl.ws_partials);
-    w.trust = (float *)(b + pl.ws_partials + pl.ws_counters);
+    w.trust = (float *)(b + pl.ws_partials);
     return w;
 }
 
@@ -224,19 +224,18 @@ int check_state(float *x, float *m, float *v, void *ws, size_t ws_bytes, const P
     return DEDLOC_OK;
 }
 
-// Pass A over every chunk, then pass B over every chunk.
+// Per chunk of tensors: pass A, the trust ratios, pass B.
 int run_lamb(int src, const Plan &pl, const PeerTable *pt, const GradArgs &ga, const LambParams &lp,
              float *x, float *m, float *v, void *ws, float *trust_out, hipStream_t s) {
     const LambWs w = carve(pl, ws);
     for (size_t c = 0; c < pl.chunks.size(); c++) {
-        // a chunk of empty tensors still runs one block to publish r = 1
-        const uint32_t grid = pl.chunk_tiles[c] ? pl.chunk_tiles[c] : 1;
-        hipError_t e = timed(K_LAMB_A_F32 + src, s, [&] { return launch_lamb_a(src, pl.chunks[c], grid, pt, ga, lp, x, m, v, w, trust_out, s); });
+        const Chunk &ch = pl.chunks[c];
+        const uint32_t tiles = pl.chunk_tiles[c];
+        hipError_t e = timed(K_LAMB_A_F32 + src, s, [&] { return launch_lamb_a(src, ch, tiles, pt, ga, lp, x, m, v, w, s); });
         if (e != hipSuccess) return hip_fail(e, "LAMB pass A launch");
-    }
-    for (size_t c = 0; c < pl.chunks.size(); c++) {
-        if (pl.chunk_tiles[c] == 0) continue;
-        hipError_t e = timed(K_LAMB_B, s, [&] { return launch_lamb_b(pl.chunks[c], pl.chunk_tiles[c], lp, x, m, v, w, s); });
+        e = timed(K_LAMB_TRUST, s, [&] { return launch_lamb_trust(ch, lp, w, trust_out, s); });
+        if (e != hipSuccess) return hip_fail(e, "LAMB trust-ratio launch");
+        e = timed(K_LAMB_B, s, [&] { return launch_lamb_b(ch, tiles, lp, x, m, v, w, s); });
         if (e != hipSuccess) return hip_fail(e, "LAMB pass B launch");
     }
     return DEDLOC_OK;

@@ -57,7 +57,6 @@ struct GradArgs {
 
 struct LambWs {
     double *partials;        // 2 per tile: sum x^2, sum u^2
-    unsigned *counters;      // per tensor: tiles finished (returns to 0)
     float *trust;            // per tensor: r_t, read by pass B
 };
 
@@ -73,7 +72,9 @@ hipError_t launch_reduce_i8(const PeerTable &pt, uint64_t len, int8_t *out, floa
                             float *mean, hipStream_t s);
 hipError_t launch_lamb_a(int src, const Chunk &ch, uint32_t n_tiles, const PeerTable *pt,
                          const GradArgs &ga, const LambParams &lp, float *x, float *m, float *v,
-                         const LambWs &ws, float *trust_out, hipStream_t s);
+                         const LambWs &ws, hipStream_t s);
+hipError_t launch_lamb_trust(const Chunk &ch, const LambParams &lp, const LambWs &ws, float *trust_out,
+                             hipStream_t s);
 hipError_t launch_lamb_b(const Chunk &ch, uint32_t n_tiles, const LambParams &lp, float *x,
                          const float *m, const float *v, const LambWs &ws, hipStream_t s);
 hipError_t launch_fill_zero(void *p, size_t bytes, hipStream_t s);

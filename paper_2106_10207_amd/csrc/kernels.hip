@@ -381,28 +381,19 @@ __device__ __forceinline__ void store8(float *p, uint64_t e0, int cnt, const flo
 }
 
 // Pass A: gradient (optionally the fused average), new moments, and the
-// per-tile sums of x^2 and u^2.  The last tile of each tensor to finish sums
-// the tensor's tile partials in tile order and publishes its trust ratio.
+// per-tile sums of x^2 and u^2 (fp64, fixed tree inside the tile).
 template <int SRC>
 __global__ __launch_bounds__(kWG) void lamb_a_kernel(const Chunk ch, const PeerTable pt,
                                                      const GradArgs ga, const LambParams lp,
                                                      const float *__restrict__ x,
                                                      float *__restrict__ m, float *__restrict__ v,
-                                                     LambWs ws, float *__restrict__ trust_out) {
-    __shared__ int s_last;
+                                                     LambWs ws) {
     const uint32_t b = blockIdx.x;
     const uint32_t k = chunk_tensor(ch, b);
     const uint64_t t_lo = ch.off[k], t_hi = ch.off[k + 1];
     const uint32_t tile = b - ch.tile_begin[k];
     const uint64_t e0 = t_lo + (uint64_t)tile * kTile + (uint64_t)threadIdx.x * kVec;
     const float lam = (ch.flags[k] & 1u) ? lp.wd : 0.0f;
-
-    if (b == 0 && threadIdx.x < ch.nt && ch.off[threadIdx.x] == ch.off[threadIdx.x + 1]) {
-        // an empty tensor has both norms 0: its ratio is 1
-        ws.trust[ch.t0 + threadIdx.x] = 1.0f;
-        if (trust_out) trust_out[ch.t0 + threadIdx.x] = 1.0f;
-    }
-    if (b >= ch.tile_begin[ch.nt]) return;  // the lone block of a chunk without tiles
 
     double sx = 0.0, su = 0.0;
     if (e0 < t_hi) {
@@ -427,26 +418,25 @@ __global__ __launch_bounds__(kWG) void lamb_a_kernel(const Chunk ch, const PeerT
         store8(m, e0, cnt, mv);
         store8(v, e0, cnt, vv);
     }
-
     block_sum2(sx, su);
-    const uint32_t ntiles = ch.tile_begin[k + 1] - ch.tile_begin[k];
-    const uint32_t first_slot = ch.tile_base + ch.tile_begin[k];
     if (threadIdx.x == 0) {
-        __hip_atomic_store(&ws.partials[2 * (ch.tile_base + b)], sx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&ws.partials[2 * (ch.tile_base + b) + 1], su, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const unsigned prev = __hip_atomic_fetch_add(&ws.counters[ch.t0 + k], 1u, __ATOMIC_ACQ_REL,
-                                                     __HIP_MEMORY_SCOPE_AGENT);
-        s_last = (prev == ntiles - 1);
+        ws.partials[2 * (ch.tile_base + b)] = sx;
+        ws.partials[2 * (ch.tile_base + b) + 1] = su;
     }
-    __syncthreads();
-    if (!s_last) return;
+}
 
-    // last tile of tensor k: fixed-order sum of its tiles' partials
-    __atomic_thread_fence(__ATOMIC_ACQUIRE);
+// Trust ratios of the chunk's tensors: block k sums tensor k's tile partials
+// in a fixed order (lane-strided, then a fixed tree), so r_t is the same on
+// every run.  Empty tensors have both norms 0 and get r = 1.
+__global__ __launch_bounds__(kWG) void lamb_trust_kernel(const Chunk ch, const LambParams lp,
+                                                         LambWs ws, float *__restrict__ trust_out) {
+    const uint32_t k = blockIdx.x;
+    const uint32_t first = ch.tile_base + ch.tile_begin[k];
+    const uint32_t ntiles = ch.tile_begin[k + 1] - ch.tile_begin[k];
     double ax = 0.0, au = 0.0;
     for (uint32_t i = threadIdx.x; i < ntiles; i += kWG) {
-        ax += __hip_atomic_load(&ws.partials[2 * (first_slot + i)], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        au += __hip_atomic_load(&ws.partials[2 * (first_slot + i) + 1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ax += ws.partials[2 * (first + i)];
+        au += ws.partials[2 * (first + i) + 1];
     }
     block_sum2(ax, au);
     if (threadIdx.x == 0) {
@@ -455,7 +445,6 @@ __global__ __launch_bounds__(kWG) void lamb_a_kernel(const Chunk ch, const PeerT
         if (!lp.unit_trust && (ch.flags[k] & 2u) && X > 0.0 && U > 0.0) r = (float)(X / U);
         ws.trust[ch.t0 + k] = r;
         if (trust_out) trust_out[ch.t0 + k] = r;
-        __hip_atomic_store(&ws.counters[ch.t0 + k], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 
@@ -531,27 +520,21 @@ hipError_t launch_reduce_i8(const PeerTable &pt, uint64_t len, int8_t *out, floa
 
 hipError_t launch_lamb_a(int src, const Chunk &ch, uint32_t n_tiles, const PeerTable *pt,
                          const GradArgs &ga, const LambParams &lp, float *x, float *m, float *v,
-                         const LambWs &ws, float *trust_out, hipStream_t s) {
+                         const LambWs &ws, hipStream_t s) {
     static const PeerTable empty = {};
     const PeerTable &p = pt ? *pt : empty;
-    const dim3 grid(n_tiles), block(kWG);
     switch (src) {
-    case kSrcF32:
-        hipLaunchKernelGGL(lamb_a_kernel<kSrcF32>, grid, block, 0, s, ch, p, ga, lp, x, m, v, ws, trust_out);
-        break;
-    case kSrcFP16:
-        hipLaunchKernelGGL(lamb_a_kernel<kSrcFP16>, grid, block, 0, s, ch, p, ga, lp, x, m, v, ws, trust_out);
-        break;
-    case kSrcI8:
-        hipLaunchKernelGGL(lamb_a_kernel<kSrcI8>, grid, block, 0, s, ch, p, ga, lp, x, m, v, ws, trust_out);
-        break;
-    case kSrcPeersFP16:
-        hipLaunchKernelGGL(lamb_a_kernel<kSrcPeersFP16>, grid, block, 0, s, ch, p, ga, lp, x, m, v, ws, trust_out);
-        break;
-    default:
-        return hipErrorInvalidValue;
+    case kSrcF32: DEDLOC_LAUNCH(dim3(n_tiles), lamb_a_kernel<kSrcF32>, s, ch, p, ga, lp, x, m, v, ws);
+    case kSrcFP16: DEDLOC_LAUNCH(dim3(n_tiles), lamb_a_kernel<kSrcFP16>, s, ch, p, ga, lp, x, m, v, ws);
+    case kSrcI8: DEDLOC_LAUNCH(dim3(n_tiles), lamb_a_kernel<kSrcI8>, s, ch, p, ga, lp, x, m, v, ws);
+    case kSrcPeersFP16: DEDLOC_LAUNCH(dim3(n_tiles), lamb_a_kernel<kSrcPeersFP16>, s, ch, p, ga, lp, x, m, v, ws);
+    default: return hipErrorInvalidValue;
     }
-    return hipGetLastError();
+}
+
+hipError_t launch_lamb_trust(const Chunk &ch, const LambParams &lp, const LambWs &ws, float *trust_out,
+                             hipStream_t s) {
+    DEDLOC_LAUNCH(dim3(ch.nt), lamb_trust_kernel, s, ch, lp, ws, trust_out);
 }
 
 hipError_t launch_lamb_b(const Chunk &ch, uint32_t n_tiles, const LambParams &lp, float *x,
