@@ -150,6 +150,8 @@ int check_tensors(uint64_t P, const uint64_t *off, uint32_t T) {
     for (uint32_t t = 0; t < T; t++) {
         if (off[t + 1] < off[t]) return fail(DEDLOC_ERR_INVALID_ARG, "tensor offsets decrease at %u", t);
         if (off[t] % kVec) return fail(DEDLOC_ERR_ALIGN, "tensor offset %u is not a multiple of 8", t);
+        if (off[t + 1] - off[t] >= (1ull << 32))
+            return fail(DEDLOC_ERR_INVALID_ARG, "tensor %u has 2^32 or more elements", t);
     }
     return DEDLOC_OK;
 }
@@ -158,29 +160,35 @@ void make_plan(uint64_t P, const uint64_t *off, const uint8_t *flags, uint32_t T
     (void)P;
     pl.chunks.clear();
     pl.chunk_tiles.clear();
-    uint32_t base = 0;
-    for (uint32_t t0 = 0; t0 < T; t0 += kChunkTensors) {
+    uint32_t base_tile = 0;
+    uint32_t t0 = 0;
+    while (t0 < T) {
         Chunk c;
         memset(&c, 0, sizeof c);
-        c.nt = (T - t0 < (uint32_t)kChunkTensors) ? T - t0 : kChunkTensors;
+        c.base = off[t0];
         c.t0 = t0;
-        c.tile_base = base;
-        uint32_t tiles = 0;
-        for (uint32_t k = 0; k < c.nt; k++) {
-            c.off[k] = off[t0 + k];
+        c.tile_base = base_tile;
+        uint32_t tiles = 0, k = 0;
+        // take tensors while they fit the table and the chunk spans < 2^32 elements
+        while (k < (uint32_t)kChunkTensors && t0 + k < T && off[t0 + k + 1] - c.base < (1ull << 32)) {
+            c.start[k] = (uint32_t)(off[t0 + k] - c.base);
             c.tile_begin[k] = tiles;
             c.flags[k] = flags ? flags[t0 + k] : 0;
             const uint64_t len = off[t0 + k + 1] - off[t0 + k];
             tiles += (uint32_t)((len + kTile - 1) / kTile);
+            k++;
         }
-        c.off[c.nt] = off[t0 + c.nt];
-        c.tile_begin[c.nt] = tiles;
+        if (k == 0) k = 1;  // unreachable: every tensor was checked to span < 2^32 elements
+        c.nt = k;
+        c.start[k] = (uint32_t)(off[t0 + k] - c.base);
+        c.tile_begin[k] = tiles;
         pl.chunks.push_back(c);
         pl.chunk_tiles.push_back(tiles);
-        base += tiles;
+        base_tile += tiles;
+        t0 += k;
     }
-    pl.n_tiles = base;
-    pl.ws_partials = round_up((size_t)base * 2 * sizeof(double), 256);
+    pl.n_tiles = base_tile;
+    pl.ws_partials = round_up((size_t)base_tile * 2 * sizeof(double), 256);
     pl.ws_trust = round_up((size_t)T * sizeof(float), 256);
     pl.ws_total = pl.ws_partials + pl.ws_trust;
 }

@@ -7,13 +7,33 @@
 
 namespace dedloc {
 
+// Launch-shape tuning (set from measurements on MI355X).
+#ifndef DEDLOC_VPL
+#define DEDLOC_VPL 1          // 8-element vectors per lane in a LAMB tile
+#endif
+#ifndef DEDLOC_PEER_BATCH
+#define DEDLOC_PEER_BATCH 16  // peer loads issued before the first fma
+#endif
+#ifndef DEDLOC_NT_PEERS
+#define DEDLOC_NT_PEERS 1     // non-temporal hint on loads of data read once
+#endif
+#ifndef DEDLOC_NT_STORES
+#define DEDLOC_NT_STORES 0    // non-temporal hint on streamed stores
+#endif
+#ifndef DEDLOC_B_REVERSE
+#define DEDLOC_B_REVERSE 1    // pass B visits tiles last-to-first (its re-reads
+                              // start with what pass A touched last)
+#endif
+
 constexpr int kWG = 256;               // threads per workgroup: 4 wave64
 constexpr int kVec = 8;                // fp32/fp16 elements per lane (16 B of fp16, 2x16 B of fp32)
-constexpr int kTile = kWG * kVec;      // LAMB tile: 2048 elements of one tensor
+constexpr int kVPL = DEDLOC_VPL;
+constexpr int kPeerBatch = DEDLOC_PEER_BATCH;
+constexpr int kTile = kWG * kVec * kVPL;  // LAMB tile: elements of one tensor per workgroup
 constexpr int kMaxPeers = 64;          // peer table lives in the kernel arguments
 constexpr int kI8Block = 1024;         // int8 codec block = one wave64 x 16 codes
 constexpr int kI8PerLane = 16;
-constexpr int kChunkTensors = 64;      // tensors described per LAMB launch
+constexpr int kChunkTensors = 192;     // tensors described per LAMB launch
 
 // Active peers (counts > 0) in ascending peer order, with their weights.
 struct PeerTable {
@@ -23,15 +43,17 @@ struct PeerTable {
     uint32_t n;
 };
 
-// A run of consecutive tensors handled by one LAMB launch.  Tiles never cross
-// a tensor: tensor k of the chunk owns launch blocks
+// A run of consecutive tensors handled by one LAMB launch (it spans fewer
+// than 2^32 elements).  Tiles never cross a tensor: tensor k of the chunk
+// covers elements base + [start[k], start[k+1]) and owns launch blocks
 // [tile_begin[k], tile_begin[k+1]).
 struct Chunk {
-    uint64_t off[kChunkTensors + 1];      // absolute element offsets
-    uint32_t tile_begin[kChunkTensors + 1];
+    uint64_t base;                        // absolute offset of the chunk's first element
     uint32_t nt;                          // tensors in this chunk
     uint32_t t0;                          // index of the chunk's first tensor
     uint32_t tile_base;                   // index of the chunk's first tile in the workspace
+    uint32_t start[kChunkTensors + 1];    // element offsets relative to base
+    uint32_t tile_begin[kChunkTensors + 1];
     uint8_t flags[kChunkTensors];
 };
 

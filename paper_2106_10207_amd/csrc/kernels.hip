@@ -16,6 +16,18 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------- helpers
 
+// Loads of data read once (peer messages) and stores of data written once.
+template <typename T>
+__device__ __forceinline__ T ld_stream(const T *p) {
+    if (DEDLOC_NT_PEERS) return __builtin_nontemporal_load(p);
+    return *p;
+}
+template <typename T>
+__device__ __forceinline__ void st_stream(T *p, T v) {
+    if (DEDLOC_NT_STORES) __builtin_nontemporal_store(v, p);
+    else *p = v;
+}
+
 __device__ __forceinline__ float h2f(unsigned bits) {
     return (float)__builtin_bit_cast(_Float16, (uint16_t)bits);
 }
@@ -101,9 +113,9 @@ __global__ __launch_bounds__(kWG) void encode_fp16_kernel(const float *__restric
                                                           uint16_t *__restrict__ codes) {
     const uint64_t e0 = ((uint64_t)blockIdx.x * kWG + threadIdx.x) * kVec;
     if (e0 + kVec <= n) {
-        const f32x4 a = *(const f32x4 *)(x + e0), b = *(const f32x4 *)(x + e0 + 4);
+        const f32x4 a = ld_stream((const f32x4 *)(x + e0)), b = ld_stream((const f32x4 *)(x + e0 + 4));
         float v[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
-        *(u32x4 *)(codes + e0) = pack_fp16x8(v);
+        st_stream((u32x4 *)(codes + e0), pack_fp16x8(v));
     } else {
         for (uint64_t e = e0; e < n; e++) codes[e] = (uint16_t)f2h(x[e]);
     }
@@ -135,7 +147,7 @@ __global__ __launch_bounds__(kWG) void encode_i8_kernel(const float *__restrict_
     if (e0 + kI8PerLane <= n) {
 #pragma unroll
         for (int q = 0; q < 4; q++) {
-            const f32x4 a = *(const f32x4 *)(x + e0 + 4 * q);
+            const f32x4 a = ld_stream((const f32x4 *)(x + e0 + 4 * q));
             val[4 * q] = a[0]; val[4 * q + 1] = a[1]; val[4 * q + 2] = a[2]; val[4 * q + 3] = a[3];
         }
     } else {
@@ -178,12 +190,12 @@ __global__ __launch_bounds__(kWG) void decode_i8_kernel(const int8_t *__restrict
 __device__ __forceinline__ void reduce_fp16x8(const PeerTable &pt, uint64_t e0, float *acc) {
 #pragma unroll
     for (int i = 0; i < 8; i++) acc[i] = 0.0f;
-    constexpr int B = 8;  // peer loads kept in flight per lane
+    constexpr int B = kPeerBatch;  // peer loads kept in flight per lane
     for (uint32_t p0 = 0; p0 < pt.n; p0 += B) {
         u32x4 c[B];
 #pragma unroll
         for (int j = 0; j < B; j++)
-            if (p0 + j < pt.n) c[j] = *(const u32x4 *)((const uint16_t *)pt.codes[p0 + j] + e0);
+            if (p0 + j < pt.n) c[j] = ld_stream((const u32x4 *)((const uint16_t *)pt.codes[p0 + j] + e0));
 #pragma unroll
         for (int j = 0; j < B; j++) {
             if (p0 + j < pt.n) {
@@ -248,7 +260,7 @@ __global__ __launch_bounds__(kWG) void reduce_i8_kernel(const PeerTable pt, uint
                 const int8_t *src = (const int8_t *)pt.codes[p0 + j];
                 s[j] = pt.scales[p0 + j][blk];
                 if (full) {
-                    c[j] = *(const u32x4 *)(src + e0);
+                    c[j] = ld_stream((const u32x4 *)(src + e0));
                 } else {
                     c[j] = u32x4{0u, 0u, 0u, 0u};
                     for (int k = 0; k < kI8PerLane; k++)
@@ -330,7 +342,7 @@ __device__ __forceinline__ void load_grad(const GradArgs &ga, const PeerTable &p
             float acc[8];
             reduce_fp16x8(pt, e0, acc);
             const u32x4 c = pack_fp16x8(acc);
-            *(u32x4 *)(ga.out_codes + e0) = c;
+            st_stream((u32x4 *)(ga.out_codes + e0), c);
             if (ga.out_mean) {
                 *(f32x4 *)(ga.out_mean + e0) = f32x4{acc[0], acc[1], acc[2], acc[3]};
                 *(f32x4 *)(ga.out_mean + e0 + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
@@ -373,8 +385,8 @@ __device__ __forceinline__ void load8(const float *p, uint64_t e0, int cnt, floa
 
 __device__ __forceinline__ void store8(float *p, uint64_t e0, int cnt, const float *o) {
     if (cnt == kVec) {
-        *(f32x4 *)(p + e0) = f32x4{o[0], o[1], o[2], o[3]};
-        *(f32x4 *)(p + e0 + 4) = f32x4{o[4], o[5], o[6], o[7]};
+        st_stream((f32x4 *)(p + e0), f32x4{o[0], o[1], o[2], o[3]});
+        st_stream((f32x4 *)(p + e0 + 4), f32x4{o[4], o[5], o[6], o[7]});
     } else {
         for (int j = 0; j < cnt; j++) p[e0 + j] = o[j];
     }
@@ -390,33 +402,36 @@ __global__ __launch_bounds__(kWG) void lamb_a_kernel(const Chunk ch, const PeerT
                                                      LambWs ws) {
     const uint32_t b = blockIdx.x;
     const uint32_t k = chunk_tensor(ch, b);
-    const uint64_t t_lo = ch.off[k], t_hi = ch.off[k + 1];
+    const uint64_t t_lo = ch.base + ch.start[k], t_hi = ch.base + ch.start[k + 1];
     const uint32_t tile = b - ch.tile_begin[k];
-    const uint64_t e0 = t_lo + (uint64_t)tile * kTile + (uint64_t)threadIdx.x * kVec;
     const float lam = (ch.flags[k] & 1u) ? lp.wd : 0.0f;
 
     double sx = 0.0, su = 0.0;
-    if (e0 < t_hi) {
-        const int cnt = (int)(t_hi - e0 < (uint64_t)kVec ? t_hi - e0 : (uint64_t)kVec);
-        float g[8], xv[8], mv[8], vv[8];
-        load_grad<SRC>(ga, pt, e0, cnt, g);
-        load8(x, e0, cnt, xv);
-        load8(m, e0, cnt, mv);
-        load8(v, e0, cnt, vv);
 #pragma unroll
-        for (int j = 0; j < 8; j++) {
-            const float mn = fmaf(lp.beta1, mv[j], lp.omb1 * g[j]);
-            const float vn = fmaf(lp.beta2, vv[j], lp.omb2 * (g[j] * g[j]));
-            const float u = lamb_dir(mn, vn, xv[j], lam, lp);
-            mv[j] = mn;
-            vv[j] = vn;
-            if (j < cnt) {
-                sx += (double)xv[j] * (double)xv[j];
-                su += (double)u * (double)u;
+    for (int r = 0; r < kVPL; r++) {
+        const uint64_t e0 = t_lo + (uint64_t)tile * kTile + ((uint64_t)r * kWG + threadIdx.x) * kVec;
+        if (e0 < t_hi) {
+            const int cnt = (int)(t_hi - e0 < (uint64_t)kVec ? t_hi - e0 : (uint64_t)kVec);
+            float g[8], xv[8], mv[8], vv[8];
+            load8(x, e0, cnt, xv);
+            load8(m, e0, cnt, mv);
+            load8(v, e0, cnt, vv);
+            load_grad<SRC>(ga, pt, e0, cnt, g);
+#pragma unroll
+            for (int j = 0; j < 8; j++) {
+                const float mn = fmaf(lp.beta1, mv[j], lp.omb1 * g[j]);
+                const float vn = fmaf(lp.beta2, vv[j], lp.omb2 * (g[j] * g[j]));
+                const float u = lamb_dir(mn, vn, xv[j], lam, lp);
+                mv[j] = mn;
+                vv[j] = vn;
+                if (j < cnt) {
+                    sx += (double)xv[j] * (double)xv[j];
+                    su += (double)u * (double)u;
+                }
             }
+            store8(m, e0, cnt, mv);
+            store8(v, e0, cnt, vv);
         }
-        store8(m, e0, cnt, mv);
-        store8(v, e0, cnt, vv);
     }
     block_sum2(sx, su);
     if (threadIdx.x == 0) {
@@ -433,10 +448,22 @@ __global__ __launch_bounds__(kWG) void lamb_trust_kernel(const Chunk ch, const L
     const uint32_t k = blockIdx.x;
     const uint32_t first = ch.tile_base + ch.tile_begin[k];
     const uint32_t ntiles = ch.tile_begin[k + 1] - ch.tile_begin[k];
+    typedef double f64x2 __attribute__((ext_vector_type(2)));
+    const f64x2 *part = (const f64x2 *)ws.partials + first;
     double ax = 0.0, au = 0.0;
-    for (uint32_t i = threadIdx.x; i < ntiles; i += kWG) {
-        ax += ws.partials[2 * (first + i)];
-        au += ws.partials[2 * (first + i) + 1];
+    constexpr int U = 8;  // loads in flight per lane
+    for (uint32_t i0 = 0; i0 < ntiles; i0 += U * kWG) {
+        f64x2 q[U];
+#pragma unroll
+        for (int j = 0; j < U; j++) {
+            const uint32_t i = i0 + j * kWG + threadIdx.x;
+            q[j] = i < ntiles ? part[i] : f64x2{0.0, 0.0};
+        }
+#pragma unroll
+        for (int j = 0; j < U; j++) {
+            ax += q[j][0];
+            au += q[j][1];
+        }
     }
     block_sum2(ax, au);
     if (threadIdx.x == 0) {
@@ -454,21 +481,25 @@ __global__ __launch_bounds__(kWG) void lamb_b_kernel(const Chunk ch, const LambP
                                                      float *__restrict__ x,
                                                      const float *__restrict__ m,
                                                      const float *__restrict__ v, LambWs ws) {
-    const uint32_t b = blockIdx.x;
+    const uint32_t b = DEDLOC_B_REVERSE ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
     const uint32_t k = chunk_tensor(ch, b);
-    const uint64_t t_hi = ch.off[k + 1];
-    const uint64_t e0 = ch.off[k] + (uint64_t)(b - ch.tile_begin[k]) * kTile + (uint64_t)threadIdx.x * kVec;
-    if (e0 >= t_hi) return;
-    const int cnt = (int)(t_hi - e0 < (uint64_t)kVec ? t_hi - e0 : (uint64_t)kVec);
+    const uint64_t t_hi = ch.base + ch.start[k + 1];
+    const uint64_t base = ch.base + ch.start[k] + (uint64_t)(b - ch.tile_begin[k]) * kTile;
     const float lam = (ch.flags[k] & 1u) ? lp.wd : 0.0f;
     const float lrr = lp.lr * ws.trust[ch.t0 + k];
-    float xv[8], mv[8], vv[8];
-    load8(x, e0, cnt, xv);
-    load8(m, e0, cnt, mv);
-    load8(v, e0, cnt, vv);
 #pragma unroll
-    for (int j = 0; j < 8; j++) xv[j] = xv[j] - lrr * lamb_dir(mv[j], vv[j], xv[j], lam, lp);
-    store8(x, e0, cnt, xv);
+    for (int r = 0; r < kVPL; r++) {
+        const uint64_t e0 = base + ((uint64_t)r * kWG + threadIdx.x) * kVec;
+        if (e0 >= t_hi) break;
+        const int cnt = (int)(t_hi - e0 < (uint64_t)kVec ? t_hi - e0 : (uint64_t)kVec);
+        float xv[8], mv[8], vv[8];
+        load8(x, e0, cnt, xv);
+        load8(m, e0, cnt, mv);
+        load8(v, e0, cnt, vv);
+#pragma unroll
+        for (int j = 0; j < 8; j++) xv[j] = xv[j] - lrr * lamb_dir(mv[j], vv[j], xv[j], lam, lp);
+        store8(x, e0, cnt, xv);
+    }
 }
 
 __global__ __launch_bounds__(kWG) void fill_zero_kernel(uint32_t *p, uint64_t n_words) {
@@ -491,11 +522,11 @@ static inline unsigned grid_for(uint64_t items, uint64_t per_block) {
     } while (0)
 
 hipError_t launch_encode_fp16(const float *x, uint64_t n, uint16_t *codes, hipStream_t s) {
-    DEDLOC_LAUNCH(dim3(grid_for(n, kTile)), encode_fp16_kernel, s, x, n, codes);
+    DEDLOC_LAUNCH(dim3(grid_for(n, (uint64_t)kWG * kVec)), encode_fp16_kernel, s, x, n, codes);
 }
 
 hipError_t launch_decode_fp16(const uint16_t *codes, uint64_t n, float *out, hipStream_t s) {
-    DEDLOC_LAUNCH(dim3(grid_for(n, kTile)), decode_fp16_kernel, s, codes, n, out);
+    DEDLOC_LAUNCH(dim3(grid_for(n, (uint64_t)kWG * kVec)), decode_fp16_kernel, s, codes, n, out);
 }
 
 hipError_t launch_encode_i8(const float *x, uint64_t n, int8_t *codes, float *scales, hipStream_t s) {
@@ -509,7 +540,7 @@ hipError_t launch_decode_i8(const int8_t *codes, const float *scales, uint64_t n
 
 hipError_t launch_reduce_fp16(const PeerTable &pt, uint64_t len, uint16_t *out, float *mean,
                               hipStream_t s) {
-    DEDLOC_LAUNCH(dim3(grid_for(len, kTile)), reduce_fp16_kernel, s, pt, len, out, mean);
+    DEDLOC_LAUNCH(dim3(grid_for(len, (uint64_t)kWG * kVec)), reduce_fp16_kernel, s, pt, len, out, mean);
 }
 
 hipError_t launch_reduce_i8(const PeerTable &pt, uint64_t len, int8_t *out, float *out_scales,

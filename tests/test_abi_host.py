@@ -167,3 +167,25 @@ def test_round_validation_before_launch():
     assert call([0, 3000, 1000, P]) == D.DEDLOC_ERR_INVALID_ARG       # decreasing
     ps = (ctypes.c_void_p * 2)(A, A)
     assert call([0, 1000, P], D.DEDLOC_CODEC_I8, 1024, ps, A) == D.DEDLOC_ERR_INVALID_ARG  # not on a block
+
+
+def _ws_expected(sizes, tile=2048):
+    tiles = sum((n + tile - 1) // tile for n in sizes)
+    r = lambda v: (v + 255) // 256 * 256
+    return r(tiles * 16) + r(len(sizes) * 4)
+
+
+@pytest.mark.parametrize("sizes", [
+    [3_000_000_000, 3_000_000_000, 8],       # launches split where a chunk would span 2^32 elements
+    [64] * 500 + [100],                      # more tensors than one launch describes
+    [0, 0, 8, 0],                            # empty tensors own no tiles
+])
+def test_workspace_bytes_large_tables(sizes):
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.uint64)
+    assert D.dedloc_lamb_workspace_bytes(int(off[-1]), off) == _ws_expected(sizes)
+
+
+def test_workspace_rejects_huge_tensor():
+    off = np.array([0, 1 << 32], np.uint64)
+    with pytest.raises(D.DedlocError):
+        D.dedloc_lamb_workspace_bytes(1 << 32, off)
