@@ -37,7 +37,80 @@ def _parse():
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES, 10 times "
                          "(calibrates HBM byte counters), then exit")
+    ap.add_argument("--summarize-counters", metavar="DIR", default=None,
+                    help="only turn the rocprofv3 counter runs under DIR (pmc_FETCH_SIZE, "
+                         "pmc_WRITE_SIZE, pmc_copy_FETCH_SIZE, pmc_copy_WRITE_SIZE) into "
+                         "profiles/traffic_<kernel>_<workload>.json, then exit")
     return ap.parse_args()
+
+
+# rocprofv3 kernel names -> the library's kernel kinds
+KERNEL_KINDS = {
+    "dedloc::encode_fp16_kernel": "encode_fp16",
+    "dedloc::encode_i8_kernel": "encode_i8",
+    "dedloc::decode_fp16_kernel": "decode_fp16",
+    "dedloc::decode_i8_kernel": "decode_i8",
+    "dedloc::reduce_fp16_kernel": "reduce_fp16",
+    "dedloc::reduce_i8_kernel": "reduce_i8",
+    "void dedloc::lamb_a_kernel<0>": "lamb_a_f32",
+    "void dedloc::lamb_a_kernel<1>": "lamb_a_fp16",
+    "void dedloc::lamb_a_kernel<2>": "lamb_a_i8",
+    "void dedloc::lamb_a_kernel<3>": "lamb_a_fused_fp16",
+    "dedloc::lamb_trust_kernel": "lamb_trust",
+    "dedloc::lamb_b_kernel": "lamb_b",
+}
+
+COUNTER_COMMANDS = (
+    "timeout -s KILL 120 rocprofv3 --pmc {c} --output-format csv -d DIR/pmc_{c} -o run -- "
+    "python3 bench.py --workload {w} --steps 5 --warmup 1 --no-cpu-baseline",
+    "timeout -s KILL 60 rocprofv3 --pmc {c} --output-format csv -d DIR/pmc_copy_{c} -o run -- "
+    "python3 bench.py --copy-probe 268435456",
+)
+
+
+def summarize_counters(root_dir, workload):
+    """Per-kernel HBM bytes per launch from FETCH_SIZE and WRITE_SIZE (KiB per
+    dispatch), each scaled by the ratio of known bytes to the counter's
+    reading for a plain 256 MiB device copy."""
+    import csv
+    import hashlib
+    from collections import defaultdict
+
+    def per_kernel(d):
+        acc = defaultdict(list)
+        for r in csv.DictReader(open(os.path.join(root_dir, d, "run_counter_collection.csv"))):
+            acc[r["Kernel_Name"].split("(")[0]].append(float(r["Counter_Value"]))
+        return {k: sum(v) / len(v) for k, v in acc.items()}
+
+    copy_bytes = 268435456
+    scale = {}
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        cp = per_kernel(f"pmc_copy_{c}")
+        copy_kib = max(cp.values())  # the copy kernel
+        scale[c] = copy_bytes / (copy_kib * 1024.0)
+    fetch, write = per_kernel("pmc_FETCH_SIZE"), per_kernel("pmc_WRITE_SIZE")
+    root = os.path.dirname(os.path.abspath(__file__))
+    digest = hashlib.sha256(open(os.path.join(root, "paper_2106_10207_amd", "csrc", "kernels.hip"),
+                                 "rb").read()).hexdigest()
+    written = []
+    for name, kind in KERNEL_KINDS.items():
+        if name not in fetch or name not in write:
+            continue
+        fb = fetch[name] * 1024.0 * scale["FETCH_SIZE"]
+        wb = write[name] * 1024.0 * scale["WRITE_SIZE"]
+        rec = {
+            "kernel": kind, "workload": workload,
+            "fetch_kib_per_launch_raw": fetch[name], "write_kib_per_launch_raw": write[name],
+            "copy_calibration": {"bytes": copy_bytes, "fetch_scale": scale["FETCH_SIZE"],
+                                 "write_scale": scale["WRITE_SIZE"]},
+            "hbm_bytes_per_launch": fb + wb, "read_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+            "commands": [c.format(c=k, w=workload) for c in COUNTER_COMMANDS for k in ("FETCH_SIZE", "WRITE_SIZE")],
+            "kernels_hip_sha256": digest,
+        }
+        out = os.path.join(root, "profiles", f"traffic_{kind}_{workload}.json")
+        json.dump(rec, open(out, "w"), indent=1)
+        written.append(out)
+    return written
 
 
 def kernel_roofline(dr, prof, steps):
@@ -157,6 +230,11 @@ def main():
     from paper_2106_10207_amd import dedloc as D
     from paper_2106_10207_amd import harness as H
     from paper_2106_10207_amd import workloads as W
+
+    if args.summarize_counters:
+        for f in summarize_counters(args.summarize_counters, args.workload):
+            print(f)
+        return
 
     if args.copy_probe:
         a = torch.ones(args.copy_probe // 4, device="cuda")
