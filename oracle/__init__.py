@@ -11,7 +11,9 @@ Functions and the passages they follow:
   encode_*/decode_* - the build's wire codecs (fp16 RNE; int8 absmax/127)
   reduce     - Section 3.2 (a reducer averages its partition from all senders)
   lamb       - Section 3.1 and the XL appendix (LAMB, layer-wise trust ratio)
+  lars       - Section 4.1 (SwAV trains with LARS: layer-wise rate scaling)
   round      - Sections 3.1-3.2 (reduce-scatter, gather, one optimizer step)
+  round_lars - the same round with the LARS step
 """
 
 from __future__ import annotations
@@ -51,6 +53,12 @@ class _LambCfg(ctypes.Structure):
                 ("force_unit_trust", ctypes.c_int32)]
 
 
+class _LarsCfg(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("momentum", ctypes.c_float),
+                ("trust_coef", ctypes.c_float), ("weight_decay", ctypes.c_float),
+                ("force_unit_trust", ctypes.c_int32)]
+
+
 _lib = None
 
 
@@ -75,6 +83,10 @@ def _L():
         _lib.oracle_round.argtypes = [vp, vp, vp, u32, vp, u32, ctypes.c_int, u32,
                                       vp, vp, vp, vp, vp, u64, vp, vp, u32,
                                       ctypes.POINTER(_LambCfg), vp, vp, vp]
+        _lib.oracle_lars.argtypes = [vp, vp, vp, u64, vp, vp, u32, ctypes.POINTER(_LarsCfg), vp]
+        _lib.oracle_round_lars.argtypes = [vp, vp, vp, u32, vp, u32, ctypes.c_int, u32,
+                                           vp, vp, vp, vp, u64, vp, vp, u32,
+                                           ctypes.POINTER(_LarsCfg), vp, vp, vp]
     return _lib
 
 
@@ -224,3 +236,55 @@ def round_(peer_codes, counts, bounds, codec, x, m, v, offsets, flags, cfg,
                            T, ctypes.byref(cfg), _p(trust), _p(mean), _p(scratch))
     _check(rc)
     return dict(codes=out, scales=osc, mean=mean, x=x, m=m, v=v, trust=trust)
+
+
+def lars_cfg(lr=4.8, momentum=0.9, trust_coef=1e-3, weight_decay=1e-6,
+             force_unit_trust=False) -> _LarsCfg:
+    return _LarsCfg(lr, momentum, trust_coef, weight_decay, int(force_unit_trust))
+
+
+def lars(x, v, g, offsets, flags, cfg: _LarsCfg):
+    """One LARS step; returns new (x, v, trust)."""
+    x = _c(x, np.float32).copy()
+    v = _c(v, np.float32).copy()
+    g = _c(g, np.float32)
+    off = _c(offsets, np.uint64)
+    fl = _c(flags, np.uint8)
+    T = len(fl)
+    trust = np.empty(T, dtype=np.float32)
+    _check(_L().oracle_lars(_p(x), _p(v), _p(g), x.size, _p(off), _p(fl), T,
+                            ctypes.byref(cfg), _p(trust)))
+    return x, v, trust
+
+
+def round_lars(peer_codes, counts, bounds, codec, x, v, offsets, flags, cfg: _LarsCfg,
+               peer_scales=None, block=1024):
+    """One averaging round followed by a LARS step.
+
+    Returns dict(codes, scales, mean, x, v, trust)."""
+    n = len(peer_codes)
+    P = x.size
+    pc = [np.ascontiguousarray(a) for a in peer_codes]
+    ps = None if peer_scales is None else [_c(s, np.float32) for s in peer_scales]
+    cnt = _c(counts, np.uint32)
+    bnd = _c(bounds, np.uint64)
+    x = _c(x, np.float32).copy()
+    v = _c(v, np.float32).copy()
+    off = _c(offsets, np.uint64)
+    fl = _c(flags, np.uint8)
+    T = len(fl)
+    if codec == CODEC_FP16:
+        out = np.empty(P, dtype=np.uint16)
+        osc = None
+    else:
+        out = np.empty(P, dtype=np.int8)
+        osc = np.empty((P + block - 1) // block, dtype=np.float32)
+    trust = np.empty(T, dtype=np.float32)
+    mean = np.empty(P, dtype=np.float32)
+    scratch = np.empty(3 * max(P, 1), dtype=np.float32)
+    rc = _L().oracle_round_lars(_ptr_array(pc), None if ps is None else _ptr_array(ps),
+                                _p(cnt), n, _p(bnd), len(bnd) - 1, codec, block,
+                                _p(out), _p(osc), _p(x), _p(v), P, _p(off), _p(fl), T,
+                                ctypes.byref(cfg), _p(trust), _p(mean), _p(scratch))
+    _check(rc)
+    return dict(codes=out, scales=osc, mean=mean, x=x, v=v, trust=trust)

@@ -275,6 +275,51 @@ int oracle_lamb(float *x, float *m, float *v, const float *g, uint64_t P,
 }
 
 /* ------------------------------------------------------------------------ */
+/* LARS step (Section 4.1 trains SwAV with LARS).  The update is the published
+ * LARS algorithm (layer-wise adaptive rate scaling with momentum, learning
+ * rate folded into the momentum buffer):
+ *   r = eta*||x_t|| / (||g_t|| + lambda_t*||x_t||) per tensor t (1 if either
+ *       norm is 0, the tensor is not adaptive, or force_unit_trust)
+ *   v' = mu*v + (lr*r) * (g + lambda_t*x),   x' = x - v'
+ * Roundings: d = g + lambda*x (product then sum), s = lr*r (fp32),
+ * v' = fmaf(mu, v, s*d), x' = x - v'; the norms accumulate exact double
+ * squares in double in element order; r is evaluated in double from the
+ * norms and rounded once to fp32. */
+typedef struct {
+    float lr, momentum, trust_coef, weight_decay;
+    int32_t force_unit_trust;
+} oracle_lars_cfg;
+
+int oracle_lars(float *x, float *v, const float *g, uint64_t P, const uint64_t *off,
+                const uint8_t *flags, uint32_t T, const oracle_lars_cfg *cfg, float *trust)
+{
+    if (T == 0 || off[0] != 0 || off[T] != P) return OR_EINVAL;
+    for (uint32_t t = 0; t < T; t++)
+        if (off[t + 1] < off[t]) return OR_EINVAL;
+    for (uint32_t t = 0; t < T; t++) {
+        float lam = (flags[t] & 1) ? cfg->weight_decay : 0.0f;
+        double sx = 0.0, sg = 0.0;
+        for (uint64_t e = off[t]; e < off[t + 1]; e++) {
+            sx += (double)x[e] * (double)x[e];
+            sg += (double)g[e] * (double)g[e];
+        }
+        double X = sqrt(sx), G = sqrt(sg);
+        float r = 1.0f;
+        if (!cfg->force_unit_trust && (flags[t] & 2) && X > 0.0 && G > 0.0)
+            r = (float)((double)cfg->trust_coef * X / (G + (double)lam * X));
+        if (trust) trust[t] = r;
+        float s = cfg->lr * r;
+        for (uint64_t e = off[t]; e < off[t + 1]; e++) {
+            float d = g[e] + lam * x[e];
+            float vn = fmaf(cfg->momentum, v[e], s * d);
+            v[e] = vn;
+            x[e] = x[e] - vn;
+        }
+    }
+    return OR_OK;
+}
+
+/* ------------------------------------------------------------------------ */
 /* One whole round as a peer sees it (Section 3.1: accumulate, exchange,
  * one optimizer step; Section 3.2: reduce-scatter by shards, then gather).
  * Every shard k of `bounds` is reduced from the N peers' full-vector
@@ -317,5 +362,23 @@ int oracle_round(const void *const *peer_codes, const float *const *peer_scales,
         decode_any(codec, (const char *)out_codes + b0 * cb,
                    codec == 2 ? out_scales + b0 / blk : NULL, b1 - b0, blk, ghat + b0);
     }
+    if (!cfg) return OR_OK; /* reduce-scatter and gather only: ghat = scratch + 2P */
     return oracle_lamb(x, m, v, ghat, P, off, flags, T, cfg, trust, scratch);
+}
+
+/* The same round with the LARS step in place of LAMB (SwAV, Section 4.1);
+ * v is the momentum buffer.  `scratch` holds 3*P floats. */
+int oracle_round_lars(const void *const *peer_codes, const float *const *peer_scales,
+                      const uint32_t *counts, uint32_t n_peers, const uint64_t *bounds,
+                      uint32_t n_shards, int codec, uint32_t block, void *out_codes,
+                      float *out_scales, float *x, float *v, uint64_t P,
+                      const uint64_t *off, const uint8_t *flags, uint32_t T,
+                      const oracle_lars_cfg *cfg, float *trust, float *out_mean,
+                      float *scratch)
+{
+    int rc = oracle_round(peer_codes, peer_scales, counts, n_peers, bounds, n_shards, codec,
+                          block, out_codes, out_scales, x, NULL, v, P, off, flags, T, NULL,
+                          trust, out_mean, scratch);
+    if (rc != OR_OK) return rc;
+    return oracle_lars(x, v, scratch + 2 * P, P, off, flags, T, cfg, trust);
 }
