@@ -32,6 +32,8 @@ def _parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="albert_large")
+    ap.add_argument("--optimizer", default="lamb", choices=["lamb", "lars"],
+                    help="optimizer after the gather: LAMB (ALBERT runs) or LARS (SwAV runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-reps", type=int, default=2)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -52,12 +54,20 @@ KERNEL_KINDS = {
     "dedloc::decode_i8_kernel": "decode_i8",
     "dedloc::reduce_fp16_kernel": "reduce_fp16",
     "dedloc::reduce_i8_kernel": "reduce_i8",
-    "void dedloc::lamb_a_kernel<0>": "lamb_a_f32",
-    "void dedloc::lamb_a_kernel<1>": "lamb_a_fp16",
-    "void dedloc::lamb_a_kernel<2>": "lamb_a_i8",
-    "void dedloc::lamb_a_kernel<3>": "lamb_a_fused_fp16",
-    "dedloc::lamb_trust_kernel": "lamb_trust",
-    "dedloc::lamb_b_kernel": "lamb_b",
+    "void dedloc::opt_a_kernel<0, 0>": "lamb_a_f32",
+    "void dedloc::opt_a_kernel<1, 0>": "lamb_a_fp16",
+    "void dedloc::opt_a_kernel<2, 0>": "lamb_a_i8",
+    "void dedloc::opt_a_kernel<3, 0>": "lamb_a_fused_fp16",
+    "void dedloc::opt_trust_kernel<0>": "lamb_trust",
+    "void dedloc::opt_b_kernel<0, 0>": "lamb_b",
+    "void dedloc::opt_a_kernel<0, 1>": "lars_a_f32",
+    "void dedloc::opt_a_kernel<1, 1>": "lars_a_fp16",
+    "void dedloc::opt_a_kernel<2, 1>": "lars_a_i8",
+    "void dedloc::opt_a_kernel<3, 1>": "lars_a_fused_fp16",
+    "void dedloc::opt_trust_kernel<1>": "lars_trust",
+    "void dedloc::opt_b_kernel<0, 1>": "lars_b",
+    "void dedloc::opt_b_kernel<1, 1>": "lars_b",
+    "void dedloc::opt_b_kernel<2, 1>": "lars_b",
 }
 
 COUNTER_COMMANDS = (
@@ -122,6 +132,9 @@ def kernel_roofline(dr, prof, steps):
       reduce_i8:         N*b*P peer reads + b*P code/scale writes
       lamb_a_i8:         b*P code reads + 20P (x, m, v reads; m', v' writes)
       lamb_b:            12P reads (x, m', v') + 4P writes
+      lars_a_fused_fp16: N*b*P peer reads + b*P code writes + 4P reads of x
+      lars_a_i8:         b*P code reads + 4P reads of x
+      lars_b:            b*P code reads + 8P reads (x, v) + 8P writes (x', v')
       encode_fp16 / encode_i8: 4P reads + b*P writes"""
     wl = dr.wl
     P = wl.P
@@ -133,6 +146,10 @@ def kernel_roofline(dr, prof, steps):
         "lamb_a_i8": (b + 20.0) * P,
         "lamb_a_fp16": (b + 20.0) * P,
         "lamb_b": 16.0 * P,
+        "lars_a_fused_fp16": (n_act * b + b + 4.0) * P,
+        "lars_a_i8": (b + 4.0) * P,
+        "lars_a_fp16": (b + 4.0) * P,
+        "lars_b": (b + 16.0) * P,
         "encode_fp16": (4.0 + b) * P,
         "encode_i8": (4.0 + b) * P,
     }
@@ -195,7 +212,10 @@ def cpu_baseline(wl, dr, reps):
             local_grad = g
         del g
     x, m, v = (t.cpu().numpy() for t in W.optimizer_state(wl, "cuda"))
-    cfg = oracle.lamb_cfg(wl.lr, wl.beta1, wl.beta2, wl.eps, wl.weight_decay, step=wl.step)
+    if dr.optimizer == "lamb":
+        cfg = oracle.lamb_cfg(wl.lr, wl.beta1, wl.beta2, wl.eps, wl.weight_decay, step=wl.step)
+    else:
+        cfg = oracle.lars_cfg(wl.lars_lr, wl.lars_momentum, wl.lars_trust_coef, wl.lars_weight_decay)
     bw = W.bandwidth_weights(wl)
     times = []
     for _ in range(reps):
@@ -205,8 +225,12 @@ def cpu_baseline(wl, dr, reps):
             oracle.encode_fp16(local_grad)
         else:
             oracle.encode_i8(local_grad, 1024)
-        oracle.round_(codes, dr.counts, bounds, codec, x, m, v, wl.offsets(), wl.flags(), cfg,
-                      scales or None, 1024)
+        if dr.optimizer == "lamb":
+            oracle.round_(codes, dr.counts, bounds, codec, x, m, v, wl.offsets(), wl.flags(), cfg,
+                          scales or None, 1024)
+        else:
+            oracle.round_lars(codes, dr.counts, bounds, codec, x, m, wl.offsets(), wl.flags(), cfg,
+                              scales or None, 1024)
         times.append(time.perf_counter() - t0)
     t = float(np.mean(times))
     return {
@@ -248,7 +272,7 @@ def main():
     wl = W.WORKLOADS[args.workload]
     torch.cuda.set_device(0)
     D.load()
-    dr = H.DeviceRound(wl, "cuda", keep_local_grad=True)
+    dr = H.DeviceRound(wl, "cuda", keep_local_grad=True, optimizer=args.optimizer)
     bw = W.bandwidth_weights(wl)
 
     def step():
@@ -322,6 +346,7 @@ def main():
             "active_peers": int(np.count_nonzero(dr.counts)),
             "wire": wl.codec,
             "shards": wl.n_shards,
+            "optimizer": args.optimizer,
             "parallelism": "single GPU; peers are HBM regions",
         },
         "params_per_s": round(wl.P / t, 1),

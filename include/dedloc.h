@@ -67,6 +67,13 @@ typedef struct {
     int32_t force_unit_trust;
 } dedloc_lamb_cfg;
 
+/* LARS hyper-parameters (host struct).  force_unit_trust != 0 replaces every
+ * rate ratio by 1 (the step is then SGD with momentum). */
+typedef struct {
+    float lr, momentum, trust_coef, weight_decay;
+    int32_t force_unit_trust;
+} dedloc_lars_cfg;
+
 /* Library version (major*10000 + minor*100 + patch). */
 int dedloc_version(void);
 
@@ -133,7 +140,8 @@ int dedloc_reduce_shard(const void *const *peer_codes, const float *const *peer_
                         int32_t codec, uint32_t block, void *out_codes,
                         float *out_scales, float *out_mean, void *stream);
 
-/* Workspace for dedloc_lamb_step / dedloc_round with this tensor table
+/* Workspace for dedloc_lamb_step / dedloc_round (and the LARS
+ * counterparts dedloc_lars_step / dedloc_round_lars) with this tensor table
  * (offsets: host, n_tensors+1): two fp64 partial sums per 2048-element tile
  * and one fp32 trust ratio per tensor.  Returns 0 for an invalid table.
  * Its contents need no initialisation and carry nothing between calls;
@@ -169,6 +177,22 @@ int dedloc_lamb_step(float *x, float *m, float *v, const void *grad,
                      uint32_t n_tensors, const dedloc_lamb_cfg *cfg, float *trust_out,
                      void *ws, size_t ws_bytes, void *stream);
 
+/* One LARS step over a flat parameter buffer (Section 4.1 trains SwAV with
+ * LARS), with the published LARS update (layer-wise rate, momentum buffer
+ * holding the learning rate):
+ *   r_t = eta*||x_t|| / (||g_t|| + lambda_t*||x_t||), or 1 if either norm is
+ *         0, the tensor lacks DEDLOC_TENSOR_ADAPT, or force_unit_trust is set
+ *         (evaluated in double from fp64 norms, rounded once to fp32)
+ *   d = g + lambda_t*x;  v' = fma(mu, v, (lr*r_t)*d);  x' = x - v'
+ * eta = trust_coef, mu = momentum, lambda_t as for LAMB.
+ *   x, v  fp32[P] (v is the momentum buffer), updated in place;
+ *   grad, grad_scales, grad_codec, offsets, flags, trust_out, workspace: as
+ *   for dedloc_lamb_step (the workspace size is the same). */
+int dedloc_lars_step(float *x, float *v, const void *grad, const float *grad_scales,
+                     int32_t grad_codec, uint32_t block, uint64_t P, const uint64_t *offsets,
+                     const uint8_t *flags, uint32_t n_tensors, const dedloc_lars_cfg *cfg,
+                     float *trust_out, void *ws, size_t ws_bytes, void *stream);
+
 /* One whole averaging round as seen by one GPU holding every reducer
  * (Sections 3.1-3.2): each shard [bounds[k], bounds[k+1]) of the vector is
  * averaged from the n_peers messages (as dedloc_reduce_shard), the encoded
@@ -189,6 +213,17 @@ int dedloc_round(const void *const *peer_codes, const float *const *peer_scales,
                  const uint64_t *offsets, const uint8_t *flags, uint32_t n_tensors,
                  const dedloc_lamb_cfg *cfg, float *trust_out, float *out_mean,
                  void *ws, size_t ws_bytes, void *stream);
+
+/* The same round with the LARS step (dedloc_lars_step) in place of LAMB;
+ * v is the momentum buffer.  The fp16 path reads each peer byte once; pass B
+ * reads the gathered message, x and v again. */
+int dedloc_round_lars(const void *const *peer_codes, const float *const *peer_scales,
+                      const uint32_t *counts, uint32_t n_peers, const uint64_t *bounds,
+                      uint32_t n_shards, int32_t codec, uint32_t block, void *out_codes,
+                      float *out_scales, float *x, float *v, uint64_t P,
+                      const uint64_t *offsets, const uint8_t *flags, uint32_t n_tensors,
+                      const dedloc_lars_cfg *cfg, float *trust_out, float *out_mean,
+                      void *ws, size_t ws_bytes, void *stream);
 
 /* Per-kernel timing (tracing support for benchmarks).  Between
  * dedloc_profile_begin() and dedloc_profile_end() every kernel the library

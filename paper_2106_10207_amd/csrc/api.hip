@@ -39,12 +39,14 @@ bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
 // ------------------------------------------------------------ profiling
 enum Kind {
     K_ENCODE_FP16, K_DECODE_FP16, K_ENCODE_I8, K_DECODE_I8, K_REDUCE_FP16, K_REDUCE_I8,
-    K_LAMB_A_F32, K_LAMB_A_FP16, K_LAMB_A_I8, K_LAMB_A_FUSED_FP16, K_LAMB_TRUST, K_LAMB_B, K_FILL,
-    K_COUNT
+    K_LAMB_A_F32, K_LAMB_A_FP16, K_LAMB_A_I8, K_LAMB_A_FUSED_FP16, K_LAMB_TRUST, K_LAMB_B,
+    K_LARS_A_F32, K_LARS_A_FP16, K_LARS_A_I8, K_LARS_A_FUSED_FP16, K_LARS_TRUST, K_LARS_B,
+    K_FILL, K_COUNT
 };
 const char *const kKindNames[K_COUNT] = {
     "encode_fp16", "decode_fp16", "encode_i8", "decode_i8", "reduce_fp16", "reduce_i8",
     "lamb_a_f32", "lamb_a_fp16", "lamb_a_i8", "lamb_a_fused_fp16", "lamb_trust", "lamb_b",
+    "lars_a_f32", "lars_a_fp16", "lars_a_i8", "lars_a_fused_fp16", "lars_trust", "lars_b",
     "fill_zero"};
 
 struct Profiler {
@@ -201,30 +203,43 @@ LambWs carve(const Plan &pl, void *ws) {
     return w;
 }
 
-int make_params(const dedloc_lamb_cfg *cfg, LambParams &lp) {
+int lamb_params(const dedloc_lamb_cfg *cfg, OptParams &op) {
     if (!cfg) return fail(DEDLOC_ERR_INVALID_ARG, "cfg must not be NULL");
     if (cfg->step == 0) return fail(DEDLOC_ERR_INVALID_ARG, "step must be >= 1");
-    lp.lr = cfg->lr;
-    lp.beta1 = cfg->beta1;
-    lp.beta2 = cfg->beta2;
-    lp.omb1 = 1.0f - cfg->beta1;
-    lp.omb2 = 1.0f - cfg->beta2;
-    lp.c1 = 1.0f;
-    lp.c2 = 1.0f;
+    memset(&op, 0, sizeof op);
+    op.lr = cfg->lr;
+    op.wd = cfg->weight_decay;
+    op.beta1 = cfg->beta1;
+    op.beta2 = cfg->beta2;
+    op.omb1 = 1.0f - cfg->beta1;
+    op.omb2 = 1.0f - cfg->beta2;
+    op.c1 = 1.0f;
+    op.c2 = 1.0f;
     if (cfg->bias_correction) {
-        lp.c1 = (float)(1.0 - pow((double)cfg->beta1, (double)cfg->step));
-        lp.c2 = (float)(1.0 - pow((double)cfg->beta2, (double)cfg->step));
+        op.c1 = (float)(1.0 - pow((double)cfg->beta1, (double)cfg->step));
+        op.c2 = (float)(1.0 - pow((double)cfg->beta2, (double)cfg->step));
     }
-    lp.eps = cfg->eps;
-    lp.wd = cfg->weight_decay;
-    lp.unit_trust = cfg->force_unit_trust ? 1 : 0;
+    op.eps = cfg->eps;
+    op.unit_trust = cfg->force_unit_trust ? 1 : 0;
     return DEDLOC_OK;
 }
 
-int check_state(float *x, float *m, float *v, void *ws, size_t ws_bytes, const Plan &pl) {
-    if (!x || !m || !v) return fail(DEDLOC_ERR_INVALID_ARG, "x, m and v must not be NULL");
-    if (!aligned(x, 16) || !aligned(m, 16) || !aligned(v, 16))
-        return fail(DEDLOC_ERR_ALIGN, "x, m and v must be 16-byte aligned");
+int lars_params(const dedloc_lars_cfg *cfg, OptParams &op) {
+    if (!cfg) return fail(DEDLOC_ERR_INVALID_ARG, "cfg must not be NULL");
+    memset(&op, 0, sizeof op);
+    op.lr = cfg->lr;
+    op.wd = cfg->weight_decay;
+    op.momentum = cfg->momentum;
+    op.trust_coef = cfg->trust_coef;
+    op.unit_trust = cfg->force_unit_trust ? 1 : 0;
+    return DEDLOC_OK;
+}
+
+// x and the optimizer state (m and v for LAMB, the momentum v for LARS).
+int check_state(int opt, float *x, float *m, float *v, void *ws, size_t ws_bytes, const Plan &pl) {
+    if (!x || !v || (opt == kOptLamb && !m)) return fail(DEDLOC_ERR_INVALID_ARG, "parameter and state buffers must not be NULL");
+    if (!aligned(x, 16) || !aligned(v, 16) || (m && !aligned(m, 16)))
+        return fail(DEDLOC_ERR_ALIGN, "parameter and state buffers must be 16-byte aligned");
     if (!ws || ws_bytes < pl.ws_total)
         return fail(DEDLOC_ERR_WORKSPACE, "workspace of %zu bytes needed (got %zu)", pl.ws_total,
                     ws ? ws_bytes : (size_t)0);
@@ -232,21 +247,97 @@ int check_state(float *x, float *m, float *v, void *ws, size_t ws_bytes, const P
     return DEDLOC_OK;
 }
 
-// Per chunk of tensors: pass A, the trust ratios, pass B.
-int run_lamb(int src, const Plan &pl, const PeerTable *pt, const GradArgs &ga, const LambParams &lp,
-             float *x, float *m, float *v, void *ws, float *trust_out, hipStream_t s) {
+int grad_src(int32_t codec) {
+    return codec == DEDLOC_CODEC_F32 ? kSrcF32 : codec == DEDLOC_CODEC_FP16 ? kSrcFP16 : kSrcI8;
+}
+
+// Per chunk of tensors: pass A (gradient from src_a), the trust ratios,
+// pass B (LARS reads the gradient again from src_b).
+int run_opt(int opt, int src_a, int src_b, const Plan &pl, const PeerTable *pt, const GradArgs &ga_a,
+            const GradArgs &ga_b, const OptParams &op, float *x, float *m, float *v, void *ws,
+            float *trust_out, hipStream_t s) {
     const LambWs w = carve(pl, ws);
+    const int k_a = (opt == kOptLamb ? K_LAMB_A_F32 : K_LARS_A_F32) + src_a;
+    const int k_t = opt == kOptLamb ? K_LAMB_TRUST : K_LARS_TRUST;
+    const int k_b = opt == kOptLamb ? K_LAMB_B : K_LARS_B;
     for (size_t c = 0; c < pl.chunks.size(); c++) {
         const Chunk &ch = pl.chunks[c];
         const uint32_t tiles = pl.chunk_tiles[c];
-        hipError_t e = timed(K_LAMB_A_F32 + src, s, [&] { return launch_lamb_a(src, ch, tiles, pt, ga, lp, x, m, v, w, s); });
-        if (e != hipSuccess) return hip_fail(e, "LAMB pass A launch");
-        e = timed(K_LAMB_TRUST, s, [&] { return launch_lamb_trust(ch, lp, w, trust_out, s); });
-        if (e != hipSuccess) return hip_fail(e, "LAMB trust-ratio launch");
-        e = timed(K_LAMB_B, s, [&] { return launch_lamb_b(ch, tiles, lp, x, m, v, w, s); });
-        if (e != hipSuccess) return hip_fail(e, "LAMB pass B launch");
+        hipError_t e = timed(k_a, s, [&] { return launch_opt_a(opt, src_a, ch, tiles, pt, ga_a, op, x, m, v, w, s); });
+        if (e != hipSuccess) return hip_fail(e, "optimizer pass A launch");
+        e = timed(k_t, s, [&] { return launch_opt_trust(opt, ch, op, w, trust_out, s); });
+        if (e != hipSuccess) return hip_fail(e, "trust-ratio launch");
+        e = timed(k_b, s, [&] { return launch_opt_b(opt, src_b, ch, tiles, ga_b, op, x, m, v, w, s); });
+        if (e != hipSuccess) return hip_fail(e, "optimizer pass B launch");
     }
     return DEDLOC_OK;
+}
+
+// Validation shared by the LAMB and LARS steps.
+int prepare_step(int opt, float *x, float *m, float *v, const void *grad, const float *grad_scales,
+                 int32_t grad_codec, uint32_t block, uint64_t P, const uint64_t *offsets,
+                 const uint8_t *flags, uint32_t n_tensors, void *ws, size_t ws_bytes, Plan &pl) {
+    int rc = check_codec(grad_codec, block, true);
+    if (rc) return rc;
+    rc = check_tensors(P, offsets, n_tensors);
+    if (rc) return rc;
+    if (!flags) return fail(DEDLOC_ERR_INVALID_ARG, "flags must not be NULL");
+    make_plan(P, offsets, flags, n_tensors, pl);
+    rc = check_state(opt, x, m, v, ws, ws_bytes, pl);
+    if (rc) return rc;
+    if (!grad || !aligned(grad, 16)) return fail(DEDLOC_ERR_ALIGN, "grad must be non-NULL and 16-byte aligned");
+    if (grad_codec == DEDLOC_CODEC_I8 && (!grad_scales || !aligned(grad_scales, 4)))
+        return fail(DEDLOC_ERR_INVALID_ARG, "int8 gradient needs aligned grad_scales");
+    return DEDLOC_OK;
+}
+
+// Validation shared by the LAMB and LARS rounds.
+int prepare_round(int opt, const void *const *peer_codes, const float *const *peer_scales,
+                  const uint32_t *counts, uint32_t n_peers, const uint64_t *bounds, uint32_t n_shards,
+                  int32_t codec, uint32_t block, void *out_codes, float *out_scales, float *x, float *m,
+                  float *v, uint64_t P, const uint64_t *offsets, const uint8_t *flags, uint32_t n_tensors,
+                  float *out_mean, void *ws, size_t ws_bytes, PeerTable &pt, Plan &pl) {
+    int rc = check_codec(codec, block, false);
+    if (rc) return rc;
+    rc = build_peers(peer_codes, peer_scales, counts, n_peers, codec, pt);
+    if (rc) return rc;
+    if (!bounds || n_shards == 0) return fail(DEDLOC_ERR_INVALID_ARG, "bounds must list n_shards >= 1 shards");
+    if (bounds[0] != 0 || bounds[n_shards] != P) return fail(DEDLOC_ERR_INVALID_ARG, "shard bounds must tile [0, P)");
+    for (uint32_t k = 0; k < n_shards; k++) {
+        if (bounds[k + 1] < bounds[k]) return fail(DEDLOC_ERR_INVALID_ARG, "shard bounds decrease at %u", k);
+        if (codec == DEDLOC_CODEC_I8 && k > 0 && bounds[k] % block)
+            return fail(DEDLOC_ERR_INVALID_ARG, "int8 shard bound %u is not a multiple of the block", k);
+    }
+    rc = check_tensors(P, offsets, n_tensors);
+    if (rc) return rc;
+    if (!flags) return fail(DEDLOC_ERR_INVALID_ARG, "flags must not be NULL");
+    make_plan(P, offsets, flags, n_tensors, pl);
+    rc = check_state(opt, x, m, v, ws, ws_bytes, pl);
+    if (rc) return rc;
+    if (!out_codes || !aligned(out_codes, 16)) return fail(DEDLOC_ERR_ALIGN, "out_codes must be non-NULL and 16-byte aligned");
+    if (out_mean && !aligned(out_mean, 16)) return fail(DEDLOC_ERR_ALIGN, "out_mean must be 16-byte aligned");
+    if (codec == DEDLOC_CODEC_I8 && (!out_scales || !aligned(out_scales, 4)))
+        return fail(DEDLOC_ERR_INVALID_ARG, "int8 round needs aligned out_scales");
+    return DEDLOC_OK;
+}
+
+// The round after validation: the reduce-scatter and gather, then the
+// optimizer.  fp16: the codec is elementwise, so every shard's average is the
+// same function of the element index and pass A fuses the average of all
+// shards.  int8: interior shard bounds sit on block boundaries, so every
+// shard's blocks are the vector's blocks and one reduce launch covers all
+// shards before the optimizer reads the gathered message.
+int run_round(int opt, const PeerTable &pt, int32_t codec, void *out_codes, float *out_scales, float *x,
+              float *m, float *v, uint64_t P, const Plan &pl, const OptParams &op, float *trust_out,
+              float *out_mean, void *ws, hipStream_t s) {
+    const GradArgs gathered = {out_codes, out_scales, nullptr, nullptr};
+    if (codec == DEDLOC_CODEC_FP16) {
+        const GradArgs fused = {nullptr, nullptr, (uint16_t *)out_codes, out_mean};
+        return run_opt(opt, kSrcPeersFP16, kSrcFP16, pl, &pt, fused, gathered, op, x, m, v, ws, trust_out, s);
+    }
+    hipError_t e = timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(pt, P, (int8_t *)out_codes, out_scales, out_mean, s); });
+    if (e != hipSuccess) return hip_fail(e, "reduce launch");
+    return run_opt(opt, kSrcI8, kSrcI8, pl, nullptr, gathered, gathered, op, x, m, v, ws, trust_out, s);
 }
 
 }  // namespace
@@ -370,24 +461,32 @@ int dedloc_lamb_step(float *x, float *m, float *v, const void *grad, const float
                      int32_t grad_codec, uint32_t block, uint64_t P, const uint64_t *offsets,
                      const uint8_t *flags, uint32_t n_tensors, const dedloc_lamb_cfg *cfg,
                      float *trust_out, void *ws, size_t ws_bytes, void *stream) {
-    int rc = check_codec(grad_codec, block, true);
-    if (rc) return rc;
-    rc = check_tensors(P, offsets, n_tensors);
-    if (rc) return rc;
-    if (!flags) return fail(DEDLOC_ERR_INVALID_ARG, "flags must not be NULL");
-    LambParams lp;
-    rc = make_params(cfg, lp);
+    OptParams op;
+    int rc = lamb_params(cfg, op);
     if (rc) return rc;
     Plan pl;
-    make_plan(P, offsets, flags, n_tensors, pl);
-    rc = check_state(x, m, v, ws, ws_bytes, pl);
+    rc = prepare_step(kOptLamb, x, m, v, grad, grad_scales, grad_codec, block, P, offsets, flags, n_tensors,
+                      ws, ws_bytes, pl);
     if (rc) return rc;
-    if (!grad || !aligned(grad, 16)) return fail(DEDLOC_ERR_ALIGN, "grad must be non-NULL and 16-byte aligned");
-    if (grad_codec == DEDLOC_CODEC_I8 && (!grad_scales || !aligned(grad_scales, 4)))
-        return fail(DEDLOC_ERR_INVALID_ARG, "int8 gradient needs aligned grad_scales");
-    GradArgs ga = {grad, grad_scales, nullptr, nullptr};
-    const int src = grad_codec == DEDLOC_CODEC_F32 ? kSrcF32 : grad_codec == DEDLOC_CODEC_FP16 ? kSrcFP16 : kSrcI8;
-    return run_lamb(src, pl, nullptr, ga, lp, x, m, v, ws, trust_out, (hipStream_t)stream);
+    const GradArgs ga = {grad, grad_scales, nullptr, nullptr};
+    const int src = grad_src(grad_codec);
+    return run_opt(kOptLamb, src, src, pl, nullptr, ga, ga, op, x, m, v, ws, trust_out, (hipStream_t)stream);
+}
+
+int dedloc_lars_step(float *x, float *v, const void *grad, const float *grad_scales, int32_t grad_codec,
+                     uint32_t block, uint64_t P, const uint64_t *offsets, const uint8_t *flags,
+                     uint32_t n_tensors, const dedloc_lars_cfg *cfg, float *trust_out, void *ws,
+                     size_t ws_bytes, void *stream) {
+    OptParams op;
+    int rc = lars_params(cfg, op);
+    if (rc) return rc;
+    Plan pl;
+    rc = prepare_step(kOptLars, x, nullptr, v, grad, grad_scales, grad_codec, block, P, offsets, flags,
+                      n_tensors, ws, ws_bytes, pl);
+    if (rc) return rc;
+    const GradArgs ga = {grad, grad_scales, nullptr, nullptr};
+    const int src = grad_src(grad_codec);
+    return run_opt(kOptLars, src, src, pl, nullptr, ga, ga, op, x, nullptr, v, ws, trust_out, (hipStream_t)stream);
 }
 
 int dedloc_round(const void *const *peer_codes, const float *const *peer_scales, const uint32_t *counts,
@@ -396,44 +495,36 @@ int dedloc_round(const void *const *peer_codes, const float *const *peer_scales,
                  const uint64_t *offsets, const uint8_t *flags, uint32_t n_tensors,
                  const dedloc_lamb_cfg *cfg, float *trust_out, float *out_mean, void *ws, size_t ws_bytes,
                  void *stream) {
-    int rc = check_codec(codec, block, false);
+    OptParams op;
+    int rc = lamb_params(cfg, op);
     if (rc) return rc;
     PeerTable pt;
-    rc = build_peers(peer_codes, peer_scales, counts, n_peers, codec, pt);
-    if (rc) return rc;
-    if (!bounds || n_shards == 0) return fail(DEDLOC_ERR_INVALID_ARG, "bounds must list n_shards >= 1 shards");
-    if (bounds[0] != 0 || bounds[n_shards] != P) return fail(DEDLOC_ERR_INVALID_ARG, "shard bounds must tile [0, P)");
-    for (uint32_t k = 0; k < n_shards; k++) {
-        if (bounds[k + 1] < bounds[k]) return fail(DEDLOC_ERR_INVALID_ARG, "shard bounds decrease at %u", k);
-        if (codec == DEDLOC_CODEC_I8 && k > 0 && bounds[k] % block)
-            return fail(DEDLOC_ERR_INVALID_ARG, "int8 shard bound %u is not a multiple of the block", k);
-    }
-    rc = check_tensors(P, offsets, n_tensors);
-    if (rc) return rc;
-    if (!flags) return fail(DEDLOC_ERR_INVALID_ARG, "flags must not be NULL");
-    LambParams lp;
-    rc = make_params(cfg, lp);
-    if (rc) return rc;
     Plan pl;
-    make_plan(P, offsets, flags, n_tensors, pl);
-    rc = check_state(x, m, v, ws, ws_bytes, pl);
+    rc = prepare_round(kOptLamb, peer_codes, peer_scales, counts, n_peers, bounds, n_shards, codec, block,
+                       out_codes, out_scales, x, m, v, P, offsets, flags, n_tensors, out_mean, ws, ws_bytes,
+                       pt, pl);
     if (rc) return rc;
-    if (!out_codes || !aligned(out_codes, 16)) return fail(DEDLOC_ERR_ALIGN, "out_codes must be non-NULL and 16-byte aligned");
-    if (out_mean && !aligned(out_mean, 16)) return fail(DEDLOC_ERR_ALIGN, "out_mean must be 16-byte aligned");
-    hipStream_t s = (hipStream_t)stream;
-    if (codec == DEDLOC_CODEC_FP16) {
-        // Elementwise codec: every shard's average is the same function of
-        // the element index, so the fused pass covers all shards at once.
-        GradArgs ga = {nullptr, nullptr, (uint16_t *)out_codes, out_mean};
-        return run_lamb(kSrcPeersFP16, pl, &pt, ga, lp, x, m, v, ws, trust_out, s);
-    }
-    if (!out_scales || !aligned(out_scales, 4)) return fail(DEDLOC_ERR_INVALID_ARG, "int8 round needs aligned out_scales");
-    // int8: interior shard bounds sit on block boundaries, so every shard's
-    // blocks are the vector's blocks and one pass reduces all shards.
-    hipError_t e = timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(pt, P, (int8_t *)out_codes, out_scales, out_mean, s); });
-    if (e != hipSuccess) return hip_fail(e, "reduce launch");
-    GradArgs ga = {out_codes, out_scales, nullptr, nullptr};
-    return run_lamb(kSrcI8, pl, nullptr, ga, lp, x, m, v, ws, trust_out, s);
+    return run_round(kOptLamb, pt, codec, out_codes, out_scales, x, m, v, P, pl, op, trust_out, out_mean, ws,
+                     (hipStream_t)stream);
+}
+
+int dedloc_round_lars(const void *const *peer_codes, const float *const *peer_scales, const uint32_t *counts,
+                      uint32_t n_peers, const uint64_t *bounds, uint32_t n_shards, int32_t codec,
+                      uint32_t block, void *out_codes, float *out_scales, float *x, float *v, uint64_t P,
+                      const uint64_t *offsets, const uint8_t *flags, uint32_t n_tensors,
+                      const dedloc_lars_cfg *cfg, float *trust_out, float *out_mean, void *ws,
+                      size_t ws_bytes, void *stream) {
+    OptParams op;
+    int rc = lars_params(cfg, op);
+    if (rc) return rc;
+    PeerTable pt;
+    Plan pl;
+    rc = prepare_round(kOptLars, peer_codes, peer_scales, counts, n_peers, bounds, n_shards, codec, block,
+                       out_codes, out_scales, x, nullptr, v, P, offsets, flags, n_tensors, out_mean, ws,
+                       ws_bytes, pt, pl);
+    if (rc) return rc;
+    return run_round(kOptLars, pt, codec, out_codes, out_scales, x, nullptr, v, P, pl, op, trust_out, out_mean,
+                     ws, (hipStream_t)stream);
 }
 
 int dedloc_profile_begin(uint32_t max_launches) {

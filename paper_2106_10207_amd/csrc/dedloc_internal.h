@@ -57,8 +57,17 @@ struct Chunk {
     uint8_t flags[kChunkTensors];
 };
 
-struct LambParams {
-    float lr, beta1, beta2, omb1, omb2, c1, c2, eps, wd;
+// Optimizer applied after the gather.
+enum Opt : int {
+    kOptLamb = 0,  // Adam moments + layer-wise trust ratio ||x||/||u||
+    kOptLars = 1   // momentum SGD + layer-wise rate eta*||x||/(||g|| + wd*||x||)
+};
+
+// Hyper-parameters of either optimizer (host-computed constants included).
+struct OptParams {
+    float lr, wd;
+    float beta1, beta2, omb1, omb2, c1, c2, eps;  // LAMB
+    float momentum, trust_coef;                   // LARS
     int32_t unit_trust;
 };
 
@@ -92,13 +101,14 @@ hipError_t launch_reduce_fp16(const PeerTable &pt, uint64_t len, uint16_t *out, 
                               hipStream_t s);
 hipError_t launch_reduce_i8(const PeerTable &pt, uint64_t len, int8_t *out, float *out_scales,
                             float *mean, hipStream_t s);
-hipError_t launch_lamb_a(int src, const Chunk &ch, uint32_t n_tiles, const PeerTable *pt,
-                         const GradArgs &ga, const LambParams &lp, float *x, float *m, float *v,
-                         const LambWs &ws, hipStream_t s);
-hipError_t launch_lamb_trust(const Chunk &ch, const LambParams &lp, const LambWs &ws, float *trust_out,
-                             hipStream_t s);
-hipError_t launch_lamb_b(const Chunk &ch, uint32_t n_tiles, const LambParams &lp, float *x,
-                         const float *m, const float *v, const LambWs &ws, hipStream_t s);
+hipError_t launch_opt_a(int opt, int src, const Chunk &ch, uint32_t n_tiles, const PeerTable *pt,
+                        const GradArgs &ga, const OptParams &op, float *x, float *m, float *v,
+                        const LambWs &ws, hipStream_t s);
+hipError_t launch_opt_trust(int opt, const Chunk &ch, const OptParams &op, const LambWs &ws,
+                            float *trust_out, hipStream_t s);
+hipError_t launch_opt_b(int opt, int src, const Chunk &ch, uint32_t n_tiles, const GradArgs &ga,
+                        const OptParams &op, float *x, float *m, float *v, const LambWs &ws,
+                        hipStream_t s);
 hipError_t launch_fill_zero(void *p, size_t bytes, hipStream_t s);
 
 }  // namespace dedloc

@@ -300,13 +300,13 @@ __global__ __launch_bounds__(kWG) void reduce_i8_kernel(const PeerTable pt, uint
     if ((threadIdx.x & 63) == 0) out_scales[blk] = s;
 }
 
-// ------------------------------------------------------------------- LAMB
+// ------------------------------------------------------- LAMB and LARS
 
 __device__ __forceinline__ float lamb_dir(float mn, float vn, float x, float lam,
-                                          const LambParams &lp) {
-    const float mh = mn / lp.c1;
-    const float vh = vn / lp.c2;
-    return mh / (sqrtf(vh) + lp.eps) + lam * x;
+                                          const OptParams &op) {
+    const float mh = mn / op.c1;
+    const float vh = vn / op.c2;
+    return mh / (sqrtf(vh) + op.eps) + lam * x;
 }
 
 // Tensor of launch block b: the largest k with tile_begin[k] <= b (empty
@@ -392,65 +392,81 @@ __device__ __forceinline__ void store8(float *p, uint64_t e0, int cnt, const flo
     }
 }
 
-// Pass A: gradient (optionally the fused average), new moments, and the
-// per-tile sums of x^2 and u^2 (fp64, fixed tree inside the tile).
-template <int SRC>
-__global__ __launch_bounds__(kWG) void lamb_a_kernel(const Chunk ch, const PeerTable pt,
-                                                     const GradArgs ga, const LambParams lp,
-                                                     const float *__restrict__ x,
-                                                     float *__restrict__ m, float *__restrict__ v,
-                                                     LambWs ws) {
+// Pass A.  LAMB: gradient (optionally the fused average), new moments, and
+// the per-tile sums of x^2 and u^2.  LARS: gradient (optionally the fused
+// average) and the per-tile sums of x^2 and g^2; nothing else is written.
+// Sums are fp64 with a fixed tree inside the tile.
+template <int SRC, int OPT>
+__global__ __launch_bounds__(kWG) void opt_a_kernel(const Chunk ch, const PeerTable pt,
+                                                    const GradArgs ga, const OptParams op,
+                                                    const float *__restrict__ x,
+                                                    float *__restrict__ m, float *__restrict__ v,
+                                                    LambWs ws) {
     const uint32_t b = blockIdx.x;
     const uint32_t k = chunk_tensor(ch, b);
     const uint64_t t_lo = ch.base + ch.start[k], t_hi = ch.base + ch.start[k + 1];
     const uint32_t tile = b - ch.tile_begin[k];
-    const float lam = (ch.flags[k] & 1u) ? lp.wd : 0.0f;
+    const float lam = (ch.flags[k] & 1u) ? op.wd : 0.0f;
 
-    double sx = 0.0, su = 0.0;
+    double s0 = 0.0, s1 = 0.0;
 #pragma unroll
     for (int r = 0; r < kVPL; r++) {
         const uint64_t e0 = t_lo + (uint64_t)tile * kTile + ((uint64_t)r * kWG + threadIdx.x) * kVec;
         if (e0 < t_hi) {
             const int cnt = (int)(t_hi - e0 < (uint64_t)kVec ? t_hi - e0 : (uint64_t)kVec);
-            float g[8], xv[8], mv[8], vv[8];
+            float g[8], xv[8];
             load8(x, e0, cnt, xv);
-            load8(m, e0, cnt, mv);
-            load8(v, e0, cnt, vv);
-            load_grad<SRC>(ga, pt, e0, cnt, g);
+            if (OPT == kOptLamb) {
+                float mv[8], vv[8];
+                load8(m, e0, cnt, mv);
+                load8(v, e0, cnt, vv);
+                load_grad<SRC>(ga, pt, e0, cnt, g);
 #pragma unroll
-            for (int j = 0; j < 8; j++) {
-                const float mn = fmaf(lp.beta1, mv[j], lp.omb1 * g[j]);
-                const float vn = fmaf(lp.beta2, vv[j], lp.omb2 * (g[j] * g[j]));
-                const float u = lamb_dir(mn, vn, xv[j], lam, lp);
-                mv[j] = mn;
-                vv[j] = vn;
-                if (j < cnt) {
-                    sx += (double)xv[j] * (double)xv[j];
-                    su += (double)u * (double)u;
+                for (int j = 0; j < 8; j++) {
+                    const float mn = fmaf(op.beta1, mv[j], op.omb1 * g[j]);
+                    const float vn = fmaf(op.beta2, vv[j], op.omb2 * (g[j] * g[j]));
+                    const float u = lamb_dir(mn, vn, xv[j], lam, op);
+                    mv[j] = mn;
+                    vv[j] = vn;
+                    if (j < cnt) {
+                        s0 += (double)xv[j] * (double)xv[j];
+                        s1 += (double)u * (double)u;
+                    }
+                }
+                store8(m, e0, cnt, mv);
+                store8(v, e0, cnt, vv);
+            } else {
+                load_grad<SRC>(ga, pt, e0, cnt, g);
+#pragma unroll
+                for (int j = 0; j < 8; j++) {
+                    if (j < cnt) {
+                        s0 += (double)xv[j] * (double)xv[j];
+                        s1 += (double)g[j] * (double)g[j];
+                    }
                 }
             }
-            store8(m, e0, cnt, mv);
-            store8(v, e0, cnt, vv);
         }
     }
-    block_sum2(sx, su);
+    block_sum2(s0, s1);
     if (threadIdx.x == 0) {
-        ws.partials[2 * (ch.tile_base + b)] = sx;
-        ws.partials[2 * (ch.tile_base + b) + 1] = su;
+        ws.partials[2 * (ch.tile_base + b)] = s0;
+        ws.partials[2 * (ch.tile_base + b) + 1] = s1;
     }
 }
 
 // Trust ratios of the chunk's tensors: block k sums tensor k's tile partials
 // in a fixed order (lane-strided, then a fixed tree), so r_t is the same on
 // every run.  Empty tensors have both norms 0 and get r = 1.
-__global__ __launch_bounds__(kWG) void lamb_trust_kernel(const Chunk ch, const LambParams lp,
-                                                         LambWs ws, float *__restrict__ trust_out) {
+//   LAMB: r = ||x|| / ||u||;  LARS: r = eta*||x|| / (||g|| + lambda*||x||).
+template <int OPT>
+__global__ __launch_bounds__(kWG) void opt_trust_kernel(const Chunk ch, const OptParams op,
+                                                        LambWs ws, float *__restrict__ trust_out) {
     const uint32_t k = blockIdx.x;
     const uint32_t first = ch.tile_base + ch.tile_begin[k];
     const uint32_t ntiles = ch.tile_begin[k + 1] - ch.tile_begin[k];
     typedef double f64x2 __attribute__((ext_vector_type(2)));
     const f64x2 *part = (const f64x2 *)ws.partials + first;
-    double ax = 0.0, au = 0.0;
+    double a0 = 0.0, a1 = 0.0;
     constexpr int U = 8;  // loads in flight per lane
     for (uint32_t i0 = 0; i0 < ntiles; i0 += U * kWG) {
         f64x2 q[U];
@@ -461,43 +477,65 @@ __global__ __launch_bounds__(kWG) void lamb_trust_kernel(const Chunk ch, const L
         }
 #pragma unroll
         for (int j = 0; j < U; j++) {
-            ax += q[j][0];
-            au += q[j][1];
+            a0 += q[j][0];
+            a1 += q[j][1];
         }
     }
-    block_sum2(ax, au);
+    block_sum2(a0, a1);
     if (threadIdx.x == 0) {
-        const double X = sqrt(ax), U = sqrt(au);
+        const double X = sqrt(a0), Y = sqrt(a1);
         float r = 1.0f;
-        if (!lp.unit_trust && (ch.flags[k] & 2u) && X > 0.0 && U > 0.0) r = (float)(X / U);
+        if (!op.unit_trust && (ch.flags[k] & 2u) && X > 0.0 && Y > 0.0) {
+            if (OPT == kOptLamb) {
+                r = (float)(X / Y);
+            } else {
+                const double lam = (ch.flags[k] & 1u) ? (double)op.wd : 0.0;
+                r = (float)((double)op.trust_coef * X / (Y + lam * X));
+            }
+        }
         ws.trust[ch.t0 + k] = r;
         if (trust_out) trust_out[ch.t0 + k] = r;
     }
 }
 
-// Pass B: x' = x - (lr * r_t) * u, with u recomputed from x, m', v' by the
-// same operations as pass A.
-__global__ __launch_bounds__(kWG) void lamb_b_kernel(const Chunk ch, const LambParams lp,
-                                                     float *__restrict__ x,
-                                                     const float *__restrict__ m,
-                                                     const float *__restrict__ v, LambWs ws) {
+// Pass B.  LAMB: x' = x - (lr * r_t) * u, with u recomputed from x, m', v' by
+// the same operations as pass A.  LARS: v' = fma(mu, v, (lr*r_t)*(g + lambda*x)),
+// x' = x - v', with g read again from the gathered message (SRC).
+template <int SRC, int OPT>
+__global__ __launch_bounds__(kWG) void opt_b_kernel(const Chunk ch, const GradArgs ga,
+                                                    const OptParams op, float *__restrict__ x,
+                                                    float *__restrict__ m, float *__restrict__ v,
+                                                    LambWs ws) {
     const uint32_t b = DEDLOC_B_REVERSE ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
     const uint32_t k = chunk_tensor(ch, b);
     const uint64_t t_hi = ch.base + ch.start[k + 1];
     const uint64_t base = ch.base + ch.start[k] + (uint64_t)(b - ch.tile_begin[k]) * kTile;
-    const float lam = (ch.flags[k] & 1u) ? lp.wd : 0.0f;
-    const float lrr = lp.lr * ws.trust[ch.t0 + k];
+    const float lam = (ch.flags[k] & 1u) ? op.wd : 0.0f;
+    const float lrr = op.lr * ws.trust[ch.t0 + k];
 #pragma unroll
     for (int r = 0; r < kVPL; r++) {
         const uint64_t e0 = base + ((uint64_t)r * kWG + threadIdx.x) * kVec;
         if (e0 >= t_hi) break;
         const int cnt = (int)(t_hi - e0 < (uint64_t)kVec ? t_hi - e0 : (uint64_t)kVec);
-        float xv[8], mv[8], vv[8];
+        float xv[8], vv[8];
         load8(x, e0, cnt, xv);
-        load8(m, e0, cnt, mv);
         load8(v, e0, cnt, vv);
+        if (OPT == kOptLamb) {
+            float mv[8];
+            load8(m, e0, cnt, mv);
 #pragma unroll
-        for (int j = 0; j < 8; j++) xv[j] = xv[j] - lrr * lamb_dir(mv[j], vv[j], xv[j], lam, lp);
+            for (int j = 0; j < 8; j++) xv[j] = xv[j] - lrr * lamb_dir(mv[j], vv[j], xv[j], lam, op);
+        } else {
+            float g[8];
+            load_grad<SRC>(ga, PeerTable{}, e0, cnt, g);
+#pragma unroll
+            for (int j = 0; j < 8; j++) {
+                const float d = g[j] + lam * xv[j];
+                vv[j] = fmaf(op.momentum, vv[j], lrr * d);
+                xv[j] = xv[j] - vv[j];
+            }
+            store8(v, e0, cnt, vv);
+        }
         store8(x, e0, cnt, xv);
     }
 }
@@ -549,28 +587,47 @@ hipError_t launch_reduce_i8(const PeerTable &pt, uint64_t len, int8_t *out, floa
                   out_scales, mean);
 }
 
-hipError_t launch_lamb_a(int src, const Chunk &ch, uint32_t n_tiles, const PeerTable *pt,
-                         const GradArgs &ga, const LambParams &lp, float *x, float *m, float *v,
-                         const LambWs &ws, hipStream_t s) {
-    static const PeerTable empty = {};
-    const PeerTable &p = pt ? *pt : empty;
+template <int OPT>
+static hipError_t launch_a(int src, const Chunk &ch, uint32_t n_tiles, const PeerTable &p, const GradArgs &ga,
+                           const OptParams &op, float *x, float *m, float *v, const LambWs &ws, hipStream_t s) {
     switch (src) {
-    case kSrcF32: DEDLOC_LAUNCH(dim3(n_tiles), lamb_a_kernel<kSrcF32>, s, ch, p, ga, lp, x, m, v, ws);
-    case kSrcFP16: DEDLOC_LAUNCH(dim3(n_tiles), lamb_a_kernel<kSrcFP16>, s, ch, p, ga, lp, x, m, v, ws);
-    case kSrcI8: DEDLOC_LAUNCH(dim3(n_tiles), lamb_a_kernel<kSrcI8>, s, ch, p, ga, lp, x, m, v, ws);
-    case kSrcPeersFP16: DEDLOC_LAUNCH(dim3(n_tiles), lamb_a_kernel<kSrcPeersFP16>, s, ch, p, ga, lp, x, m, v, ws);
+    case kSrcF32: DEDLOC_LAUNCH(dim3(n_tiles), (opt_a_kernel<kSrcF32, OPT>), s, ch, p, ga, op, x, m, v, ws);
+    case kSrcFP16: DEDLOC_LAUNCH(dim3(n_tiles), (opt_a_kernel<kSrcFP16, OPT>), s, ch, p, ga, op, x, m, v, ws);
+    case kSrcI8: DEDLOC_LAUNCH(dim3(n_tiles), (opt_a_kernel<kSrcI8, OPT>), s, ch, p, ga, op, x, m, v, ws);
+    case kSrcPeersFP16: DEDLOC_LAUNCH(dim3(n_tiles), (opt_a_kernel<kSrcPeersFP16, OPT>), s, ch, p, ga, op, x, m, v, ws);
     default: return hipErrorInvalidValue;
     }
 }
 
-hipError_t launch_lamb_trust(const Chunk &ch, const LambParams &lp, const LambWs &ws, float *trust_out,
-                             hipStream_t s) {
-    DEDLOC_LAUNCH(dim3(ch.nt), lamb_trust_kernel, s, ch, lp, ws, trust_out);
+hipError_t launch_opt_a(int opt, int src, const Chunk &ch, uint32_t n_tiles, const PeerTable *pt,
+                        const GradArgs &ga, const OptParams &op, float *x, float *m, float *v,
+                        const LambWs &ws, hipStream_t s) {
+    static const PeerTable empty = {};
+    const PeerTable &p = pt ? *pt : empty;
+    if (opt == kOptLamb) return launch_a<kOptLamb>(src, ch, n_tiles, p, ga, op, x, m, v, ws, s);
+    if (opt == kOptLars) return launch_a<kOptLars>(src, ch, n_tiles, p, ga, op, x, m, v, ws, s);
+    return hipErrorInvalidValue;
 }
 
-hipError_t launch_lamb_b(const Chunk &ch, uint32_t n_tiles, const LambParams &lp, float *x,
-                         const float *m, const float *v, const LambWs &ws, hipStream_t s) {
-    DEDLOC_LAUNCH(dim3(n_tiles), lamb_b_kernel, s, ch, lp, x, m, v, ws);
+hipError_t launch_opt_trust(int opt, const Chunk &ch, const OptParams &op, const LambWs &ws,
+                            float *trust_out, hipStream_t s) {
+    if (opt == kOptLamb) DEDLOC_LAUNCH(dim3(ch.nt), opt_trust_kernel<kOptLamb>, s, ch, op, ws, trust_out);
+    if (opt == kOptLars) DEDLOC_LAUNCH(dim3(ch.nt), opt_trust_kernel<kOptLars>, s, ch, op, ws, trust_out);
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_opt_b(int opt, int src, const Chunk &ch, uint32_t n_tiles, const GradArgs &ga,
+                        const OptParams &op, float *x, float *m, float *v, const LambWs &ws,
+                        hipStream_t s) {
+    if (opt == kOptLamb)
+        DEDLOC_LAUNCH(dim3(n_tiles), (opt_b_kernel<kSrcF32, kOptLamb>), s, ch, ga, op, x, m, v, ws);
+    if (opt != kOptLars) return hipErrorInvalidValue;
+    switch (src) {
+    case kSrcF32: DEDLOC_LAUNCH(dim3(n_tiles), (opt_b_kernel<kSrcF32, kOptLars>), s, ch, ga, op, x, m, v, ws);
+    case kSrcFP16: DEDLOC_LAUNCH(dim3(n_tiles), (opt_b_kernel<kSrcFP16, kOptLars>), s, ch, ga, op, x, m, v, ws);
+    case kSrcI8: DEDLOC_LAUNCH(dim3(n_tiles), (opt_b_kernel<kSrcI8, kOptLars>), s, ch, ga, op, x, m, v, ws);
+    default: return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_fill_zero(void *p, size_t bytes, hipStream_t s) {

@@ -56,6 +56,17 @@ def lamb_cfg(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-6, weight_decay=0.01, step=
                            int(bias_correction), int(force_unit_trust))
 
 
+class dedloc_lars_cfg(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("momentum", ctypes.c_float),
+                ("trust_coef", ctypes.c_float), ("weight_decay", ctypes.c_float),
+                ("force_unit_trust", ctypes.c_int32)]
+
+
+def lars_cfg(lr=4.8, momentum=0.9, trust_coef=1e-3, weight_decay=1e-6,
+             force_unit_trust=False) -> dedloc_lars_cfg:
+    return dedloc_lars_cfg(lr, momentum, trust_coef, weight_decay, int(force_unit_trust))
+
+
 _lib = None
 
 _SIGS = {
@@ -82,6 +93,15 @@ _SIGS = {
                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p,
                       ctypes.c_void_p, ctypes.c_uint32, ctypes.POINTER(dedloc_lamb_cfg), ctypes.c_void_p,
                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p], ctypes.c_int),
+    "dedloc_lars_step": ([ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                          ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32,
+                          ctypes.POINTER(dedloc_lars_cfg), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                          ctypes.c_void_p], ctypes.c_int),
+    "dedloc_round_lars": ([ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32, ctypes.c_void_p,
+                           ctypes.c_uint32, ctypes.c_int32, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p,
+                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p,
+                           ctypes.c_void_p, ctypes.c_uint32, ctypes.POINTER(dedloc_lars_cfg), ctypes.c_void_p,
+                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p], ctypes.c_int),
     "dedloc_profile_begin": ([ctypes.c_uint32], ctypes.c_int),
     "dedloc_profile_end": ([ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "dedloc_kernel_kinds": ([], ctypes.c_int),
@@ -240,12 +260,27 @@ def dedloc_lamb_step(x, m, v, grad, offsets, flags, cfg: dedloc_lamb_cfg, grad_c
     return ws
 
 
+def dedloc_lars_step(x, v, grad, offsets, flags, cfg: dedloc_lars_cfg, grad_codec: int = DEDLOC_CODEC_F32,
+                     grad_scales=None, block: int = DEDLOC_I8_BLOCK, trust_out=None, ws=None, stream=None):
+    off = _host(offsets, np.uint64)
+    fl = _host(flags, np.uint8)
+    P = x.numel()
+    if ws is None:
+        ws = make_workspace(P, off, x.device)
+    _check(load().dedloc_lars_step(_dev(x), _dev(v), _dev(grad), _dev(grad_scales), grad_codec, block, P,
+                                   _ptr(off), _ptr(fl), len(fl), ctypes.byref(cfg), _dev(trust_out),
+                                   _dev(ws), ws.numel(), _stream(stream)))
+    return ws
+
+
 class RoundCall:
-    """Pre-marshalled arguments of one dedloc_round call: building the
-    pointer arrays once keeps per-call host overhead to the C call itself."""
+    """Pre-marshalled arguments of one dedloc_round call (dedloc_round_lars
+    when `cfg` is a dedloc_lars_cfg; then `m` is unused and `v` is the
+    momentum buffer): building the pointer arrays once keeps per-call host
+    overhead to the C call itself."""
 
     def __init__(self, peer_codes, counts, bounds, codec, out_codes, x, m, v, offsets, flags,
-                 cfg: dedloc_lamb_cfg, ws, peer_scales=None, out_scales=None, trust_out=None,
+                 cfg, ws, peer_scales=None, out_scales=None, trust_out=None,
                  out_mean=None, block: int = DEDLOC_I8_BLOCK):
         self._keep = (peer_codes, peer_scales, out_codes, out_scales, x, m, v, ws, trust_out, out_mean)
         self.pc = _ptrs(peer_codes)
@@ -257,15 +292,24 @@ class RoundCall:
         self.cfg = cfg
         self.args = None
         self.codec, self.block = codec, block
-        self.out = (_dev(out_codes), _dev(out_scales), _dev(x), _dev(m), _dev(v), x.numel(),
-                    _dev(trust_out), _dev(out_mean), _dev(ws), ws.numel())
+        self.lars = isinstance(cfg, dedloc_lars_cfg)
+        self.out = (_dev(out_codes), _dev(out_scales), _dev(x), None if self.lars else _dev(m), _dev(v),
+                    x.numel(), _dev(trust_out), _dev(out_mean), _dev(ws), ws.numel())
 
     def __call__(self, stream=None):
         oc, osc, x, m, v, P, tr, om, ws, wsb = self.out
-        _check(load().dedloc_round(self.pc, self.ps, _ptr(self.cnt), len(self.cnt), _ptr(self.bnd),
-                                   len(self.bnd) - 1, self.codec, self.block, oc, osc, x, m, v, P,
-                                   _ptr(self.off), _ptr(self.fl), len(self.fl), ctypes.byref(self.cfg),
-                                   tr, om, ws, wsb, _stream(stream)))
+        lib = load()
+        if self.lars:
+            rc = lib.dedloc_round_lars(self.pc, self.ps, _ptr(self.cnt), len(self.cnt), _ptr(self.bnd),
+                                       len(self.bnd) - 1, self.codec, self.block, oc, osc, x, v, P,
+                                       _ptr(self.off), _ptr(self.fl), len(self.fl), ctypes.byref(self.cfg),
+                                       tr, om, ws, wsb, _stream(stream))
+        else:
+            rc = lib.dedloc_round(self.pc, self.ps, _ptr(self.cnt), len(self.cnt), _ptr(self.bnd),
+                                  len(self.bnd) - 1, self.codec, self.block, oc, osc, x, m, v, P,
+                                  _ptr(self.off), _ptr(self.fl), len(self.fl), ctypes.byref(self.cfg),
+                                  tr, om, ws, wsb, _stream(stream))
+        _check(rc)
 
 
 def dedloc_round(peer_codes, counts, bounds, codec: int, x, m, v, offsets, flags, cfg: dedloc_lamb_cfg,
@@ -300,3 +344,20 @@ def dedloc_profile_end():
     cnt = np.zeros(n, np.uint64)
     _check(lib.dedloc_profile_end(n, _ptr(ms), _ptr(cnt)))
     return {lib.dedloc_kernel_name(k).decode(): (float(ms[k]), int(cnt[k])) for k in range(n) if cnt[k]}
+
+
+def dedloc_round_lars(peer_codes, counts, bounds, codec: int, x, v, offsets, flags, cfg: dedloc_lars_cfg,
+                      peer_scales=None, block: int = DEDLOC_I8_BLOCK, out_codes=None, out_scales=None,
+                      trust_out=None, out_mean=None, ws=None, stream=None):
+    """One averaging round followed by a LARS step; returns (out_codes, out_scales)."""
+    import torch
+    P = x.numel()
+    if out_codes is None:
+        out_codes = torch.empty(P, dtype=torch.int16 if codec == DEDLOC_CODEC_FP16 else torch.int8, device=x.device)
+    if out_scales is None and codec == DEDLOC_CODEC_I8:
+        out_scales = torch.empty((P + block - 1) // block, dtype=torch.float32, device=x.device)
+    if ws is None:
+        ws = make_workspace(P, offsets, x.device)
+    RoundCall(peer_codes, counts, bounds, codec, out_codes, x, None, v, offsets, flags, cfg, ws, peer_scales,
+              out_scales, trust_out, out_mean, block)(stream)
+    return out_codes, out_scales

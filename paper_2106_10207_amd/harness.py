@@ -33,7 +33,7 @@ class DeviceRound:
     def __init__(self, wl: W.Workload, device="cuda", fresh: bool = False,
                  poison_zero: bool = True, step: Optional[int] = None,
                  sample_ranges: Sequence[Tuple[int, int]] = (), keep_local_grad: bool = False,
-                 with_mean: bool = False):
+                 with_mean: bool = False, optimizer: str = "lamb"):
         import torch
         self.wl = wl
         self.device = device
@@ -76,7 +76,15 @@ class DeviceRound:
         self.mean = torch.empty(P, dtype=torch.float32, device=device) if with_mean else None
         self.ws = D.make_workspace(P, self.offsets, device)
         self.step = wl.step if step is None else step
-        self.cfg = D.lamb_cfg(wl.lr, wl.beta1, wl.beta2, wl.eps, wl.weight_decay, step=self.step)
+        self.optimizer = optimizer
+        if optimizer == "lamb":
+            self.cfg = D.lamb_cfg(wl.lr, wl.beta1, wl.beta2, wl.eps, wl.weight_decay, step=self.step)
+        elif optimizer == "lars":
+            # LARS keeps one buffer: the momentum (held in m; v is unused)
+            self.cfg = D.lars_cfg(wl.lars_lr, wl.lars_momentum, wl.lars_trust_coef, wl.lars_weight_decay)
+            self.v = self.m
+        else:
+            raise ValueError(f"unknown optimizer {optimizer!r}")
         self.call = D.RoundCall(self.codes, self.counts, self.bounds, self.codec, self.out_codes,
                                 self.x, self.m, self.v, self.offsets, self.flags, self.cfg, self.ws,
                                 peer_scales=self.scales if self.codec == D.DEDLOC_CODEC_I8 else None,
@@ -103,8 +111,12 @@ class DeviceRound:
         return n_act * self.wl.P * self.wl.wire_bytes_per_elem
 
     def bytes_round(self) -> float:
+        """Compulsory bytes: peer messages, the gathered message, and the
+        optimizer state read and written once (x, m, v for LAMB; x and the
+        momentum for LARS)."""
         P = self.wl.P
-        return self.bytes_peer_input() + P * self.wl.wire_bytes_per_elem + 24.0 * P
+        state = 24.0 if self.optimizer == "lamb" else 16.0
+        return self.bytes_peer_input() + P * self.wl.wire_bytes_per_elem + state * P
 
     def bytes_encode_local(self) -> float:
         return self.wl.P * (4.0 + self.wl.wire_bytes_per_elem)

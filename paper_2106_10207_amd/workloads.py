@@ -55,6 +55,11 @@ class Workload:
     eps: float = 1e-6
     weight_decay: float = 0.01
     step: int = 10
+    # LARS (the SwAV runs' optimizer): lr, momentum, trust coefficient, decay
+    lars_lr: float = 4.8
+    lars_momentum: float = 0.9
+    lars_trust_coef: float = 1e-3
+    lars_weight_decay: float = 1e-6
 
     @property
     def P(self) -> int:

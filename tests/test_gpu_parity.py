@@ -318,7 +318,7 @@ def _sample(wl, n_tensors=3, n_blocks=8, max_len=4_300_000):
     while len(pick) < min(n_tensors, len(cand)):
         pick.add(int(rng.choice(cand)))
     nblk = (wl.P + 1023) // 1024
-    blocks = sorted(set(int(b) for b in rng.integers(0, nblk, n_blocks)) | {nblk - 1})
+    blocks = sorted(set(int(b) for b in rng.integers(0, nblk, n_blocks)) | {nblk - 1}) if n_blocks else []
     return sorted(pick), blocks
 
 
