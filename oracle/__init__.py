@@ -14,6 +14,7 @@ Functions and the passages they follow:
   lars       - Section 4.1 (SwAV trains with LARS: layer-wise rate scaling)
   round      - Sections 3.1-3.2 (reduce-scatter, gather, one optimizer step)
   round_lars - the same round with the LARS step
+  group_allreduce - Section 3.2 "Node failures" / Appendix C (group averaging)
 """
 
 from __future__ import annotations
@@ -87,6 +88,8 @@ def _L():
         _lib.oracle_round_lars.argtypes = [vp, vp, vp, u32, vp, u32, ctypes.c_int, u32,
                                            vp, vp, vp, vp, u64, vp, vp, u32,
                                            ctypes.POINTER(_LarsCfg), vp, vp, vp]
+        _lib.oracle_group_allreduce.argtypes = [vp, vp, vp, u32, u32, sz, ctypes.c_int, u32, u32,
+                                                vp, vp, vp, vp, vp, vp, vp]
     return _lib
 
 
@@ -288,3 +291,42 @@ def round_lars(peer_codes, counts, bounds, codec, x, v, offsets, flags, cfg: _La
                                 ctypes.byref(cfg), _p(trust), _p(mean), _p(scratch))
     _check(rc)
     return dict(codes=out, scales=osc, mean=mean, x=x, v=v, trust=trust)
+
+
+def group_iterations(n: int, m: int) -> int:
+    """ceil(log_m n), at least 1 (m < 2 has no grid: 1, and the C call fails)."""
+    d = 1
+    while m >= 2 and m ** d < n:
+        d += 1
+    return d
+
+
+def group_allreduce(peer_codes, counts, m: int, codec: int, peer_scales=None, block: int = 1024,
+                    iters: int = 0):
+    """Group (Moshpit) all-reduce of n peer messages in groups of m.
+
+    Returns (codes [n_out, len], scales [n_out, nblk] or None, peer_out [n])."""
+    n = len(peer_codes)
+    ln = peer_codes[0].size
+    d = group_iterations(n, m)
+    groups = m ** d // m
+    cnt = _c(counts, np.uint32)
+    pc = [np.ascontiguousarray(a) for a in peer_codes]
+    ps = None if peer_scales is None else [_c(s, np.float32) for s in peer_scales]
+    nsc = 0 if codec == CODEC_FP16 else (ln + block - 1) // block
+    cdt = np.uint16 if codec == CODEC_FP16 else np.int8
+    out = np.zeros((groups, ln), dtype=cdt)
+    osc = np.zeros((groups, max(nsc, 1)), dtype=np.float32)
+    work = np.zeros((2, groups, ln), dtype=cdt)
+    wsc = np.zeros((2, groups, max(nsc, 1)), dtype=np.float32)
+    if nsc == 0:
+        osc = np.zeros((groups, 0), np.float32)
+        wsc = np.zeros((2, groups, 0), np.float32)
+    peer_out = np.zeros(n, dtype=np.uint32)
+    n_out = ctypes.c_uint32(0)
+    scratch = np.empty(2 * max(ln, 1), dtype=np.float32)
+    rc = _L().oracle_group_allreduce(_ptr_array(pc), None if ps is None else _ptr_array(ps), _p(cnt), n, m,
+                                     ln, codec, block, iters, _p(out), _p(osc) if nsc else None, _p(peer_out),
+                                     ctypes.byref(n_out), _p(work), _p(wsc) if nsc else None, _p(scratch))
+    _check(rc)
+    return out, (osc if nsc else None), peer_out

@@ -382,3 +382,119 @@ int oracle_round_lars(const void *const *peer_codes, const float *const *peer_sc
     if (rc != OR_OK) return rc;
     return oracle_lars(x, v, scratch + 2 * P, P, off, flags, T, cfg, trust);
 }
+
+/* ------------------------------------------------------------------------ */
+/* Group (Moshpit) all-reduce (Section 3.2 "Node failures", Appendix C
+ * "Fault tolerance"): instead of one global average, peers average in
+ * groups of m, in consecutive iterations with alternating groups, so that
+ * every peer holds the global average after ceil(log_m n) iterations.
+ *
+ * The grid used here: d = max(1, ceil(log_m n)) iterations over m^d slots;
+ * slot i holds peer i (i < n), the others are empty (zero samples).  In
+ * iteration k the groups are the sets of slots whose base-m digits agree
+ * except digit k; group id = slot with digit k removed.  Each member carries
+ * a sample count (initially its own); a group whose members carry zero
+ * samples in total produces nothing, otherwise it computes the weighted
+ * average of its members' messages exactly as oracle_reduce does (members
+ * with zero samples are not read), and every member takes the encoded group
+ * average and the group's total count.
+ *
+ * `iters` = 0 runs the d iterations; a positive value runs that many (to
+ * observe the intermediate state).  Outputs: the messages of the last
+ * iteration's groups, group g at out_codes + g*len codes (and, for int8,
+ * out_scales + g*ceil(len/block)); peer_out[i] = the group whose message
+ * peer i holds (UINT32_MAX if it holds none); *n_out = number of groups of
+ * the last iteration.  `work` holds 2*m^(d-1)*len codes (plus scales) and
+ * `scratch` 2*len floats. */
+static uint32_t ipow(uint32_t m, uint32_t d)
+{
+    uint32_t r = 1;
+    for (uint32_t i = 0; i < d; i++) r *= m;
+    return r;
+}
+
+int oracle_group_allreduce(const void *const *peer_codes, const float *const *peer_scales,
+                           const uint32_t *counts, uint32_t n, uint32_t m, size_t len, int codec,
+                           uint32_t block, uint32_t iters, void *out_codes, float *out_scales,
+                           uint32_t *peer_out, uint32_t *n_out, void *work, float *work_scales,
+                           float *scratch)
+{
+    if (n == 0 || n > 1024 || m < 2) return OR_EINVAL;
+    uint64_t total = 0;
+    for (uint32_t i = 0; i < n; i++) total += counts[i];
+    if (total == 0) return OR_EZERO;
+    uint32_t d = 1;
+    while (ipow(m, d) < n) d++;
+    if (iters == 0) iters = d;
+    if (iters > d) return OR_EINVAL;
+    const uint32_t slots = ipow(m, d);
+    const uint32_t groups = slots / m;
+    const size_t cb = code_bytes(codec);
+    const uint32_t blk = codec == 1 ? 1 : block;
+    const size_t nsc = codec == 1 ? 0 : (len + blk - 1) / blk;
+
+    /* per slot: where its message is (-1: original peer message; else the
+     * group index in the previous iteration's buffer) and its count */
+    int64_t src[1024 * 16];
+    uint64_t cnt[1024 * 16];
+    if (slots > 1024 * 16) return OR_EINVAL;
+    for (uint32_t i = 0; i < slots; i++) {
+        src[i] = -1;
+        cnt[i] = i < n ? counts[i] : 0;
+    }
+    const void *mem_codes[1024];
+    const float *mem_scales[1024];
+    uint32_t mem_counts[1024];
+    for (uint32_t k = 0; k < iters; k++) {
+        const uint32_t lo = ipow(m, k); /* weight of digit k */
+        const int last = (k + 1 == iters);
+        char *dst_codes = last ? (char *)out_codes : (char *)work + (size_t)(k % 2) * groups * len * cb;
+        float *dst_scales = last ? out_scales : work_scales + (size_t)(k % 2) * groups * nsc;
+        const char *prev_codes = (const char *)work + (size_t)((k + 1) % 2) * groups * len * cb;
+        const float *prev_scales = work_scales + (size_t)((k + 1) % 2) * groups * nsc;
+        int64_t nsrc[1024 * 16];
+        uint64_t ncnt[1024 * 16];
+        for (uint32_t g = 0; g < groups; g++) {
+            /* members: slots with digit k = 0..m-1, other digits from g */
+            const uint32_t base = (g / lo) * lo * m + (g % lo);
+            uint64_t gt = 0;
+            uint32_t nm = 0;
+            for (uint32_t j = 0; j < m; j++) {
+                const uint32_t s = base + j * lo;
+                gt += cnt[s];
+            }
+            for (uint32_t j = 0; j < m; j++) {
+                const uint32_t s = base + j * lo;
+                if (cnt[s] == 0) continue;
+                if (src[s] < 0) {
+                    mem_codes[nm] = peer_codes[s];
+                    mem_scales[nm] = codec == 2 ? peer_scales[s] : NULL;
+                } else {
+                    mem_codes[nm] = prev_codes + (size_t)src[s] * len * cb;
+                    mem_scales[nm] = codec == 2 ? prev_scales + (size_t)src[s] * nsc : NULL;
+                }
+                if (cnt[s] > 0xffffffffull) return OR_EINVAL;
+                mem_counts[nm] = (uint32_t)cnt[s];
+                nm++;
+            }
+            if (gt > 0) {
+                int rc = oracle_reduce(mem_codes, codec == 2 ? mem_scales : NULL, mem_counts, nm, len,
+                                       codec, blk, dst_codes + (size_t)g * len * cb,
+                                       codec == 2 ? dst_scales + (size_t)g * nsc : NULL, NULL, scratch);
+                if (rc != OR_OK) return rc;
+            }
+            for (uint32_t j = 0; j < m; j++) {
+                const uint32_t s = base + j * lo;
+                nsrc[s] = gt > 0 ? (int64_t)g : -2;
+                ncnt[s] = gt;
+            }
+        }
+        for (uint32_t i = 0; i < slots; i++) {
+            src[i] = nsrc[i];
+            cnt[i] = ncnt[i];
+        }
+    }
+    for (uint32_t i = 0; i < n; i++) peer_out[i] = src[i] >= 0 ? (uint32_t)src[i] : 0xffffffffu;
+    *n_out = groups;
+    return OR_OK;
+}
