@@ -225,6 +225,37 @@ int dedloc_round_lars(const void *const *peer_codes, const float *const *peer_sc
                       const dedloc_lars_cfg *cfg, float *trust_out, float *out_mean,
                       void *ws, size_t ws_bytes, void *stream);
 
+/* Group (Moshpit) all-reduce (Section 3.2 "Node failures"; Appendix C):
+ * instead of one global average, peers average in groups of m = group_size
+ * over d = max(1, ceil(log_m n)) consecutive iterations, so that one failing
+ * peer only affects its group, and every peer holds the global average after
+ * d iterations.  Grid: m^d slots, slot i holds peer i (i < n) and the others
+ * are empty; in iteration k the groups are the slots whose base-m digits
+ * agree except digit k (group id = slot with digit k removed).  Each member
+ * carries a sample count (initially counts[i]); a group whose members carry
+ * zero samples produces nothing, otherwise it computes the weighted average
+ * of its members' messages exactly as dedloc_reduce_shard does (members with
+ * zero samples are not read) and every member takes the encoded group
+ * average and the group's total count.
+ *   peer_codes / peer_scales  host arrays of n_peers device messages of len
+ *                             elements (16-byte aligned);
+ *   out_codes   device, n_out messages at a stride of
+ *               round_up(len * code_bytes, 256) bytes (256-byte aligned);
+ *   out_scales  int8 only: n_out * ceil(len/1024) floats;
+ *   peer_out    host uint32[n_peers]: the output message peer i holds
+ *               (0xffffffff if it holds none);  n_out (host): m^(d-1);
+ *   ws          dedloc_group_allreduce_workspace_bytes() bytes, 256-byte
+ *               aligned (two sets of intermediate group messages).
+ * n_peers <= DEDLOC_MAX_PEERS, group_size >= 2; errors as for
+ * dedloc_reduce_shard.  One launch per iteration. */
+size_t dedloc_group_allreduce_workspace_bytes(uint32_t n_peers, uint32_t group_size, uint64_t len,
+                                              int32_t codec, uint32_t block);
+int dedloc_group_allreduce(const void *const *peer_codes, const float *const *peer_scales,
+                           const uint32_t *counts, uint32_t n_peers, uint32_t group_size,
+                           uint64_t len, int32_t codec, uint32_t block, void *out_codes,
+                           float *out_scales, uint32_t *peer_out, uint32_t *n_out, void *ws,
+                           size_t ws_bytes, void *stream);
+
 /* Per-kernel timing (tracing support for benchmarks).  Between
  * dedloc_profile_begin() and dedloc_profile_end() every kernel the library
  * enqueues is bracketed by a pair of HIP events on its stream; at most

@@ -136,6 +136,19 @@ int build_peers(const void *const *codes, const float *const *scales, const uint
     return DEDLOC_OK;
 }
 
+// A plain reduce: every active peer in one group writing `out`.
+GroupTable single_group(const PeerTable &pt, void *out, float *out_scales) {
+    GroupTable gt;
+    memset(&gt, 0, sizeof gt);
+    gt.pt = pt;
+    gt.gbegin[0] = 0;
+    gt.gbegin[1] = pt.n;
+    gt.out[0] = out;
+    gt.out_scales[0] = out_scales;
+    gt.n_groups = 1;
+    return gt;
+}
+
 // LAMB tile table: tensors in launch chunks of at most kChunkTensors.
 struct Plan {
     std::vector<Chunk> chunks;
@@ -335,9 +348,39 @@ int run_round(int opt, const PeerTable &pt, int32_t codec, void *out_codes, floa
         const GradArgs fused = {nullptr, nullptr, (uint16_t *)out_codes, out_mean};
         return run_opt(opt, kSrcPeersFP16, kSrcFP16, pl, &pt, fused, gathered, op, x, m, v, ws, trust_out, s);
     }
-    hipError_t e = timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(pt, P, (int8_t *)out_codes, out_scales, out_mean, s); });
+    const GroupTable gt = single_group(pt, out_codes, out_scales);
+    hipError_t e = timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(gt, P, out_mean, s); });
     if (e != hipSuccess) return hip_fail(e, "reduce launch");
     return run_opt(opt, kSrcI8, kSrcI8, pl, nullptr, gathered, gathered, op, x, m, v, ws, trust_out, s);
+}
+
+// Group all-reduce layout: m^d slots, m^(d-1) groups per iteration, every
+// group message at a 256-byte stride.
+struct GroupPlan {
+    uint32_t d = 0, slots = 0, groups = 0;
+    size_t code_stride = 0, scale_stride = 0;   // bytes, floats
+    size_t ws_codes = 0, ws_total = 0;          // two ping-pong sets of group messages
+};
+
+int group_plan(uint32_t n, uint32_t m, uint64_t len, int32_t codec, GroupPlan &gp) {
+    if (n == 0 || n > DEDLOC_MAX_PEERS) return fail(DEDLOC_ERR_INVALID_ARG, "n_peers must be in [1, %d]", DEDLOC_MAX_PEERS);
+    if (m < 2) return fail(DEDLOC_ERR_INVALID_ARG, "group_size must be >= 2");
+    uint32_t d = 1;
+    uint64_t slots = m;
+    while (slots < n) {
+        slots *= m;
+        d++;
+    }
+    gp.d = d;
+    gp.slots = (uint32_t)slots;
+    gp.groups = (uint32_t)(slots / m);  // < n <= 64 when d > 1, and 1 when d == 1
+    const size_t cb = codec == DEDLOC_CODEC_FP16 ? 2 : 1;
+    gp.code_stride = round_up((size_t)len * cb, 256);
+    gp.scale_stride = codec == DEDLOC_CODEC_I8 ? (size_t)((len + DEDLOC_I8_BLOCK - 1) / DEDLOC_I8_BLOCK) : 0;
+    const size_t d_prev = d > 1 ? 2 : 0;  // iterations before the last ping-pong between two sets
+    gp.ws_codes = d_prev * gp.groups * gp.code_stride;
+    gp.ws_total = gp.ws_codes + round_up(d_prev * gp.groups * gp.scale_stride * sizeof(float), 256);
+    return DEDLOC_OK;
 }
 
 }  // namespace
@@ -435,10 +478,12 @@ int dedloc_reduce_shard(const void *const *peer_codes, const float *const *peer_
     hipStream_t s = (hipStream_t)stream;
     hipError_t e;
     if (codec == DEDLOC_CODEC_FP16) {
-        e = timed(K_REDUCE_FP16, s, [&] { return launch_reduce_fp16(pt, shard_len, (uint16_t *)out_codes, out_mean, s); });
+        const GroupTable gt = single_group(pt, out_codes, nullptr);
+        e = timed(K_REDUCE_FP16, s, [&] { return launch_reduce_fp16(gt, shard_len, out_mean, s); });
     } else {
         if (!out_scales || !aligned(out_scales, 4)) return fail(DEDLOC_ERR_INVALID_ARG, "int8 reduce needs aligned out_scales");
-        e = timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(pt, shard_len, (int8_t *)out_codes, out_scales, out_mean, s); });
+        const GroupTable gt = single_group(pt, out_codes, out_scales);
+        e = timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(gt, shard_len, out_mean, s); });
     }
     return e == hipSuccess ? DEDLOC_OK : hip_fail(e, "reduce launch");
 }
@@ -525,6 +570,102 @@ int dedloc_round_lars(const void *const *peer_codes, const float *const *peer_sc
     if (rc) return rc;
     return run_round(kOptLars, pt, codec, out_codes, out_scales, x, nullptr, v, P, pl, op, trust_out, out_mean,
                      ws, (hipStream_t)stream);
+}
+
+size_t dedloc_group_allreduce_workspace_bytes(uint32_t n_peers, uint32_t group_size, uint64_t len,
+                                              int32_t codec, uint32_t block) {
+    if (check_codec(codec, block, false)) return 0;
+    GroupPlan gp;
+    if (group_plan(n_peers, group_size, len, codec, gp)) return 0;
+    return gp.ws_total > 0 ? gp.ws_total : 256;
+}
+
+int dedloc_group_allreduce(const void *const *peer_codes, const float *const *peer_scales,
+                           const uint32_t *counts, uint32_t n_peers, uint32_t group_size, uint64_t len,
+                           int32_t codec, uint32_t block, void *out_codes, float *out_scales,
+                           uint32_t *peer_out, uint32_t *n_out, void *ws, size_t ws_bytes, void *stream) {
+    int rc = check_codec(codec, block, false);
+    if (rc) return rc;
+    GroupPlan gp;
+    rc = group_plan(n_peers, group_size, len, codec, gp);
+    if (rc) return rc;
+    PeerTable all;  // validates pointers, alignment, counts (total in [1, 2^24])
+    rc = build_peers(peer_codes, peer_scales, counts, n_peers, codec, all, len > 0);
+    if (rc) return rc;
+    if (!peer_out || !n_out) return fail(DEDLOC_ERR_INVALID_ARG, "peer_out and n_out must not be NULL");
+    if (len > 0) {
+        if (!out_codes || !aligned(out_codes, 256)) return fail(DEDLOC_ERR_ALIGN, "out_codes must be non-NULL and 256-byte aligned");
+        if (codec == DEDLOC_CODEC_I8 && (!out_scales || !aligned(out_scales, 4)))
+            return fail(DEDLOC_ERR_INVALID_ARG, "int8 group all-reduce needs aligned out_scales");
+        if (gp.ws_total > 0 && (!ws || ws_bytes < gp.ws_total))
+            return fail(DEDLOC_ERR_WORKSPACE, "workspace of %zu bytes needed (got %zu)", gp.ws_total, ws ? ws_bytes : (size_t)0);
+        if (gp.ws_total > 0 && !aligned(ws, 256)) return fail(DEDLOC_ERR_ALIGN, "workspace must be 256-byte aligned");
+    }
+    const uint32_t m = group_size;
+    std::vector<int64_t> src(gp.slots, -1), nsrc(gp.slots);
+    std::vector<uint64_t> cnt(gp.slots, 0), ncnt(gp.slots);
+    for (uint32_t i = 0; i < n_peers; i++) cnt[i] = counts[i];
+    hipStream_t s = (hipStream_t)stream;
+    char *wsc = (char *)ws;
+    float *wss = (float *)(wsc + gp.ws_codes);
+    uint32_t lo = 1;  // m^k, the weight of digit k
+    for (uint32_t k = 0; k < gp.d; k++, lo *= m) {
+        const bool last = k + 1 == gp.d;
+        char *dst_c = last ? (char *)out_codes : wsc + (size_t)(k % 2) * gp.groups * gp.code_stride;
+        float *dst_s = last ? out_scales : wss + (size_t)(k % 2) * gp.groups * gp.scale_stride;
+        const char *prev_c = wsc + (size_t)((k + 1) % 2) * gp.groups * gp.code_stride;
+        const float *prev_s = wss + (size_t)((k + 1) % 2) * gp.groups * gp.scale_stride;
+        GroupTable gt;
+        memset(&gt, 0, sizeof gt);
+        gt.n_groups = gp.groups;
+        for (uint32_t g = 0; g < gp.groups; g++) {
+            const uint32_t base = (g / lo) * lo * m + (g % lo);
+            uint32_t mc[DEDLOC_MAX_PEERS];
+            uint32_t nm = 0, first = gt.pt.n;
+            uint64_t total = 0;
+            for (uint32_t j = 0; j < m; j++) {
+                const uint32_t sl = base + j * lo;
+                total += cnt[sl];
+                if (cnt[sl] == 0) continue;
+                if (gt.pt.n >= (uint32_t)kMaxPeers) return fail(DEDLOC_ERR_INVALID_ARG, "too many group members");
+                if (src[sl] < 0) {
+                    gt.pt.codes[gt.pt.n] = peer_codes[sl];
+                    gt.pt.scales[gt.pt.n] = codec == DEDLOC_CODEC_I8 ? peer_scales[sl] : nullptr;
+                } else {
+                    gt.pt.codes[gt.pt.n] = prev_c + (size_t)src[sl] * gp.code_stride;
+                    gt.pt.scales[gt.pt.n] = codec == DEDLOC_CODEC_I8 ? prev_s + (size_t)src[sl] * gp.scale_stride : nullptr;
+                }
+                mc[nm++] = (uint32_t)cnt[sl];
+                gt.pt.n++;
+            }
+            gt.gbegin[g] = first;
+            if (nm > 0) {
+                float w[DEDLOC_MAX_PEERS];
+                rc = compute_weights(mc, nm, w);
+                if (rc) return rc;
+                for (uint32_t j = 0; j < nm; j++) gt.pt.w[first + j] = w[j];
+            }
+            gt.out[g] = dst_c + (size_t)g * gp.code_stride;
+            gt.out_scales[g] = codec == DEDLOC_CODEC_I8 ? dst_s + (size_t)g * gp.scale_stride : nullptr;
+            for (uint32_t j = 0; j < m; j++) {
+                const uint32_t sl = base + j * lo;
+                nsrc[sl] = total > 0 ? (int64_t)g : -2;
+                ncnt[sl] = total;
+            }
+        }
+        gt.gbegin[gp.groups] = gt.pt.n;
+        if (len > 0) {
+            hipError_t e = codec == DEDLOC_CODEC_FP16
+                               ? timed(K_REDUCE_FP16, s, [&] { return launch_reduce_fp16(gt, len, nullptr, s); })
+                               : timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(gt, len, nullptr, s); });
+            if (e != hipSuccess) return hip_fail(e, "group reduce launch");
+        }
+        src.swap(nsrc);
+        cnt.swap(ncnt);
+    }
+    for (uint32_t i = 0; i < n_peers; i++) peer_out[i] = src[i] >= 0 ? (uint32_t)src[i] : 0xffffffffu;
+    *n_out = gp.groups;
+    return DEDLOC_OK;
 }
 
 int dedloc_profile_begin(uint32_t max_launches) {

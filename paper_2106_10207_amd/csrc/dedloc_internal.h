@@ -43,6 +43,20 @@ struct PeerTable {
     uint32_t n;
 };
 
+// Groups of peers reduced by one launch (one group for a plain shard
+// reduce; the groups of one iteration of the group all-reduce).  Group g
+// averages table entries [gbegin[g], gbegin[g+1]) (its members with samples,
+// ascending) into out[g] (and out_scales[g] for int8); an empty range
+// produces nothing.
+constexpr int kMaxGroups = 64;
+struct GroupTable {
+    PeerTable pt;
+    uint32_t gbegin[kMaxGroups + 1];
+    void *out[kMaxGroups];
+    float *out_scales[kMaxGroups];
+    uint32_t n_groups;
+};
+
 // A run of consecutive tensors handled by one LAMB launch (it spans fewer
 // than 2^32 elements).  Tiles never cross a tensor: tensor k of the chunk
 // covers elements base + [start[k], start[k+1]) and owns launch blocks
@@ -97,10 +111,8 @@ hipError_t launch_decode_fp16(const uint16_t *codes, uint64_t n, float *out, hip
 hipError_t launch_encode_i8(const float *x, uint64_t n, int8_t *codes, float *scales, hipStream_t s);
 hipError_t launch_decode_i8(const int8_t *codes, const float *scales, uint64_t n, float *out,
                             hipStream_t s);
-hipError_t launch_reduce_fp16(const PeerTable &pt, uint64_t len, uint16_t *out, float *mean,
-                              hipStream_t s);
-hipError_t launch_reduce_i8(const PeerTable &pt, uint64_t len, int8_t *out, float *out_scales,
-                            float *mean, hipStream_t s);
+hipError_t launch_reduce_fp16(const GroupTable &gt, uint64_t len, float *mean, hipStream_t s);
+hipError_t launch_reduce_i8(const GroupTable &gt, uint64_t len, float *mean, hipStream_t s);
 hipError_t launch_opt_a(int opt, int src, const Chunk &ch, uint32_t n_tiles, const PeerTable *pt,
                         const GradArgs &ga, const OptParams &op, float *x, float *m, float *v,
                         const LambWs &ws, hipStream_t s);

@@ -183,22 +183,25 @@ __global__ __launch_bounds__(kWG) void decode_i8_kernel(const int8_t *__restrict
 }
 
 // ------------------------------------------------------------- the reducer
-// mean[e] = sum over active peers (ascending) of w_p * dec_p[e], one fma per
-// peer starting from +0.
+// mean[e] = sum over the active peers of a group (ascending) of
+// w_p * dec_p[e], one fma per peer starting from +0.  A launch reduces every
+// group of a GroupTable: grid row blockIdx.y is the group.
 
-// Eight consecutive fp16 elements starting at e0 (all in range).
-__device__ __forceinline__ void reduce_fp16x8(const PeerTable &pt, uint64_t e0, float *acc) {
+// Eight consecutive fp16 elements starting at e0 (all in range), peers
+// [p_lo, p_hi) of the table.
+__device__ __forceinline__ void reduce_fp16x8(const PeerTable &pt, uint32_t p_lo, uint32_t p_hi,
+                                              uint64_t e0, float *acc) {
 #pragma unroll
     for (int i = 0; i < 8; i++) acc[i] = 0.0f;
     constexpr int B = kPeerBatch;  // peer loads kept in flight per lane
-    for (uint32_t p0 = 0; p0 < pt.n; p0 += B) {
+    for (uint32_t p0 = p_lo; p0 < p_hi; p0 += B) {
         u32x4 c[B];
 #pragma unroll
         for (int j = 0; j < B; j++)
-            if (p0 + j < pt.n) c[j] = ld_stream((const u32x4 *)((const uint16_t *)pt.codes[p0 + j] + e0));
+            if (p0 + j < p_hi) c[j] = ld_stream((const u32x4 *)((const uint16_t *)pt.codes[p0 + j] + e0));
 #pragma unroll
         for (int j = 0; j < B; j++) {
-            if (p0 + j < pt.n) {
+            if (p0 + j < p_hi) {
                 const float w = pt.w[p0 + j];
                 float d[8];
                 unpack_fp16x8(c[j], d);
@@ -209,20 +212,24 @@ __device__ __forceinline__ void reduce_fp16x8(const PeerTable &pt, uint64_t e0, 
     }
 }
 
-__device__ __forceinline__ float reduce_fp16_one(const PeerTable &pt, uint64_t e) {
+__device__ __forceinline__ float reduce_fp16_one(const PeerTable &pt, uint32_t p_lo, uint32_t p_hi,
+                                                 uint64_t e) {
     float acc = 0.0f;
-    for (uint32_t p = 0; p < pt.n; p++)
+    for (uint32_t p = p_lo; p < p_hi; p++)
         acc = fmaf(pt.w[p], h2f(((const uint16_t *)pt.codes[p])[e]), acc);
     return acc;
 }
 
-__global__ __launch_bounds__(kWG) void reduce_fp16_kernel(const PeerTable pt, uint64_t len,
-                                                          uint16_t *__restrict__ out,
+__global__ __launch_bounds__(kWG) void reduce_fp16_kernel(const GroupTable gt, uint64_t len,
                                                           float *__restrict__ mean) {
+    const uint32_t g = blockIdx.y;
+    const uint32_t p_lo = gt.gbegin[g], p_hi = gt.gbegin[g + 1];
+    if (p_lo == p_hi) return;  // a group without samples produces nothing
+    uint16_t *__restrict__ out = (uint16_t *)gt.out[g];
     const uint64_t e0 = ((uint64_t)blockIdx.x * kWG + threadIdx.x) * kVec;
     if (e0 + kVec <= len) {
         float acc[8];
-        reduce_fp16x8(pt, e0, acc);
+        reduce_fp16x8(gt.pt, p_lo, p_hi, e0, acc);
         *(u32x4 *)(out + e0) = pack_fp16x8(acc);
         if (mean) {
             *(f32x4 *)(mean + e0) = f32x4{acc[0], acc[1], acc[2], acc[3]};
@@ -230,7 +237,7 @@ __global__ __launch_bounds__(kWG) void reduce_fp16_kernel(const PeerTable pt, ui
         }
     } else {
         for (uint64_t e = e0; e < len; e++) {
-            const float a = reduce_fp16_one(pt, e);
+            const float a = reduce_fp16_one(gt.pt, p_lo, p_hi, e);
             out[e] = (uint16_t)f2h(a);
             if (mean) mean[e] = a;
         }
@@ -238,10 +245,14 @@ __global__ __launch_bounds__(kWG) void reduce_fp16_kernel(const PeerTable pt, ui
 }
 
 // One wave per 1024-element block; lane holds 16 elements.
-__global__ __launch_bounds__(kWG) void reduce_i8_kernel(const PeerTable pt, uint64_t len,
-                                                        int8_t *__restrict__ out,
-                                                        float *__restrict__ out_scales,
+__global__ __launch_bounds__(kWG) void reduce_i8_kernel(const GroupTable gt, uint64_t len,
                                                         float *__restrict__ mean) {
+    const uint32_t g = blockIdx.y;
+    const uint32_t p_lo = gt.gbegin[g], p_hi = gt.gbegin[g + 1];
+    if (p_lo == p_hi) return;  // a group without samples produces nothing
+    int8_t *__restrict__ out = (int8_t *)gt.out[g];
+    float *__restrict__ out_scales = gt.out_scales[g];
+    const PeerTable &pt = gt.pt;
     const uint64_t blk = (uint64_t)blockIdx.x * (kWG / 64) +
                          (uint64_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (blk * kI8Block >= len) return;  // whole wave past the end
@@ -251,12 +262,12 @@ __global__ __launch_bounds__(kWG) void reduce_i8_kernel(const PeerTable pt, uint
 #pragma unroll
     for (int j = 0; j < kI8PerLane; j++) acc[j] = 0.0f;
     constexpr int B = 4;
-    for (uint32_t p0 = 0; p0 < pt.n; p0 += B) {
+    for (uint32_t p0 = p_lo; p0 < p_hi; p0 += B) {
         u32x4 c[B];
         float s[B];
 #pragma unroll
         for (int j = 0; j < B; j++) {
-            if (p0 + j < pt.n) {
+            if (p0 + j < p_hi) {
                 const int8_t *src = (const int8_t *)pt.codes[p0 + j];
                 s[j] = pt.scales[p0 + j][blk];
                 if (full) {
@@ -270,7 +281,7 @@ __global__ __launch_bounds__(kWG) void reduce_i8_kernel(const PeerTable pt, uint
         }
 #pragma unroll
         for (int j = 0; j < B; j++) {
-            if (p0 + j < pt.n) {
+            if (p0 + j < p_hi) {
                 const float w = pt.w[p0 + j];
 #pragma unroll
                 for (int k = 0; k < kI8PerLane; k++) {
@@ -340,7 +351,7 @@ __device__ __forceinline__ void load_grad(const GradArgs &ga, const PeerTable &p
             for (int j = 0; j < 8; j++) g[j] = sbyte(c[j >> 2], j & 3) * s;
         } else {
             float acc[8];
-            reduce_fp16x8(pt, e0, acc);
+            reduce_fp16x8(pt, 0, pt.n, e0, acc);
             const u32x4 c = pack_fp16x8(acc);
             st_stream((u32x4 *)(ga.out_codes + e0), c);
             if (ga.out_mean) {
@@ -363,7 +374,7 @@ __device__ __forceinline__ void load_grad(const GradArgs &ga, const PeerTable &p
             } else if (SRC == kSrcI8) {
                 g[j] = (float)((const int8_t *)ga.grad)[e] * ga.scales[e / kI8Block];
             } else {
-                const float a = reduce_fp16_one(pt, e);
+                const float a = reduce_fp16_one(pt, 0, pt.n, e);
                 const unsigned c = f2h(a);
                 ga.out_codes[e] = (uint16_t)c;
                 if (ga.out_mean) ga.out_mean[e] = a;
@@ -554,7 +565,7 @@ static inline unsigned grid_for(uint64_t items, uint64_t per_block) {
 #define DEDLOC_LAUNCH(grid, kernel, ...)                                   \
     do {                                                                   \
         const dim3 g_ = (grid);                                            \
-        if (g_.x == 0) return hipSuccess; /* nothing to do */              \
+        if (g_.x == 0 || g_.y == 0) return hipSuccess; /* nothing to do */ \
         hipLaunchKernelGGL(kernel, g_, dim3(kWG), 0, __VA_ARGS__);         \
         return hipGetLastError();                                          \
     } while (0)
@@ -576,15 +587,13 @@ hipError_t launch_decode_i8(const int8_t *codes, const float *scales, uint64_t n
     DEDLOC_LAUNCH(dim3(grid_for(n, (uint64_t)kWG * kI8PerLane)), decode_i8_kernel, s, codes, scales, n, out);
 }
 
-hipError_t launch_reduce_fp16(const PeerTable &pt, uint64_t len, uint16_t *out, float *mean,
-                              hipStream_t s) {
-    DEDLOC_LAUNCH(dim3(grid_for(len, (uint64_t)kWG * kVec)), reduce_fp16_kernel, s, pt, len, out, mean);
+hipError_t launch_reduce_fp16(const GroupTable &gt, uint64_t len, float *mean, hipStream_t s) {
+    DEDLOC_LAUNCH(dim3(grid_for(len, (uint64_t)kWG * kVec), gt.n_groups), reduce_fp16_kernel, s, gt, len, mean);
 }
 
-hipError_t launch_reduce_i8(const PeerTable &pt, uint64_t len, int8_t *out, float *out_scales,
-                            float *mean, hipStream_t s) {
-    DEDLOC_LAUNCH(dim3(grid_for(len, (uint64_t)kI8Block * (kWG / 64))), reduce_i8_kernel, s, pt, len, out,
-                  out_scales, mean);
+hipError_t launch_reduce_i8(const GroupTable &gt, uint64_t len, float *mean, hipStream_t s) {
+    DEDLOC_LAUNCH(dim3(grid_for(len, (uint64_t)kI8Block * (kWG / 64)), gt.n_groups), reduce_i8_kernel, s, gt, len,
+                  mean);
 }
 
 template <int OPT>

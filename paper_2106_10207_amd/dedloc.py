@@ -102,6 +102,12 @@ _SIGS = {
                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p,
                            ctypes.c_void_p, ctypes.c_uint32, ctypes.POINTER(dedloc_lars_cfg), ctypes.c_void_p,
                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p], ctypes.c_int),
+    "dedloc_group_allreduce_workspace_bytes": ([ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int32,
+                                                ctypes.c_uint32], ctypes.c_size_t),
+    "dedloc_group_allreduce": ([ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32,
+                                ctypes.c_uint64, ctypes.c_int32, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p,
+                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p],
+                               ctypes.c_int),
     "dedloc_profile_begin": ([ctypes.c_uint32], ctypes.c_int),
     "dedloc_profile_end": ([ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "dedloc_kernel_kinds": ([], ctypes.c_int),
@@ -361,3 +367,60 @@ def dedloc_round_lars(peer_codes, counts, bounds, codec: int, x, v, offsets, fla
     RoundCall(peer_codes, counts, bounds, codec, out_codes, x, None, v, offsets, flags, cfg, ws, peer_scales,
               out_scales, trust_out, out_mean, block)(stream)
     return out_codes, out_scales
+
+
+def group_iterations(n_peers: int, group_size: int) -> int:
+    d = 1
+    while group_size >= 2 and group_size ** d < n_peers:
+        d += 1
+    return d
+
+
+class GroupAllreduce:
+    """Pre-allocated buffers and marshalled arguments of dedloc_group_allreduce
+    for fixed peers, counts and group size.  After a call, messages[g] (and
+    scales[g] for int8) is group g's output and peer_out[i] the output peer i
+    holds."""
+
+    def __init__(self, peer_codes, counts, group_size: int, length: int, codec: int, peer_scales=None,
+                 block: int = DEDLOC_I8_BLOCK, device="cuda"):
+        import torch
+        n = len(peer_codes)
+        d = group_iterations(n, group_size)
+        self.n_out = group_size ** d // group_size
+        cb = 2 if codec == DEDLOC_CODEC_FP16 else 1
+        self.stride = (length * cb + 255) // 256 * 256
+        nsc = (length + block - 1) // block if codec == DEDLOC_CODEC_I8 else 0
+        self.out = torch.empty(max(self.n_out * self.stride, 256), dtype=torch.uint8, device=device)
+        self.out_scales = (torch.empty(self.n_out * nsc, dtype=torch.float32, device=device)
+                           if codec == DEDLOC_CODEC_I8 else None)
+        nb = load().dedloc_group_allreduce_workspace_bytes(n, group_size, length, codec, block)
+        if nb == 0:
+            raise DedlocError(DEDLOC_ERR_INVALID_ARG, load().dedloc_last_error().decode())
+        self.ws = torch.empty(nb, dtype=torch.uint8, device=device)
+        dt = torch.int16 if codec == DEDLOC_CODEC_FP16 else torch.int8
+        self.messages = [self.out[g * self.stride: g * self.stride + length * cb].view(dt)
+                         for g in range(self.n_out)]
+        self.scales = ([self.out_scales[g * nsc:(g + 1) * nsc] for g in range(self.n_out)]
+                       if codec == DEDLOC_CODEC_I8 else None)
+        self.peer_out = np.zeros(n, dtype=np.uint32)
+        self._n_out = ctypes.c_uint32(0)
+        self._keep = (peer_codes, peer_scales)
+        self.pc = _ptrs(peer_codes)
+        self.ps = None if peer_scales is None else _ptrs(peer_scales)
+        self.cnt = _host(counts, np.uint32)
+        self.args = (n, group_size, length, codec, block)
+
+    def __call__(self, stream=None):
+        n, m, length, codec, block = self.args
+        _check(load().dedloc_group_allreduce(self.pc, self.ps, _ptr(self.cnt), n, m, length, codec, block,
+                                             _dev(self.out), _dev(self.out_scales), _ptr(self.peer_out),
+                                             ctypes.byref(self._n_out), _dev(self.ws), self.ws.numel(),
+                                             _stream(stream)))
+        return self
+
+
+def dedloc_group_allreduce(peer_codes, counts, group_size: int, length: int, codec: int, peer_scales=None,
+                           block: int = DEDLOC_I8_BLOCK, stream=None) -> GroupAllreduce:
+    dev = next(t.device for t in peer_codes if t is not None)
+    return GroupAllreduce(peer_codes, counts, group_size, length, codec, peer_scales, block, dev)(stream)

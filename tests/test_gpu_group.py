@@ -1,0 +1,88 @@
+"""GPU parity of dedloc_group_allreduce (group / Moshpit averaging,
+Section 3.2 "Node failures", Appendix C) against the oracle: every group
+message (codes and int8 scales) bit-identical, and the same output
+assignment of every peer."""
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2106_10207_amd import dedloc as D
+from paper_2106_10207_amd import workloads as W
+from tests.test_gpu_parity import DEV, _bits, _i8, _np, _u16, _up
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(n, L, seed, codec):
+    rng = np.random.default_rng(seed)
+    g = [((p - n / 2) * 1e-3 + rng.standard_normal(L) * 1e-3).astype(np.float32) for p in range(n)]
+    counts = rng.integers(0, 300, n).astype(np.uint32)
+    counts[rng.integers(0, n)] = 11
+    if codec == D.DEDLOC_CODEC_FP16:
+        return [oracle.encode_fp16(x) for x in g], None, counts
+    enc = [oracle.encode_i8(x, 1024) for x in g]
+    return [c for c, _ in enc], [s for _, s in enc], counts
+
+
+@pytest.mark.parametrize("codec", [D.DEDLOC_CODEC_FP16, D.DEDLOC_CODEC_I8])
+@pytest.mark.parametrize("n,m,L", [(8, 2, 5000), (9, 3, 2048 * 3 + 5), (64, 8, 4096), (10, 3, 1),
+                                   (64, 2, 3000), (30, 4, 1024 * 5 + 7), (5, 8, 777), (1, 2, 100)])
+def test_group_allreduce(codec, n, m, L):
+    codes, scales, counts = _inputs(n, L, n * 100 + m, codec)
+    dc = []
+    ds = []
+    for p in range(n):
+        c = _up(codes[p].view(np.int16) if codec == D.DEDLOC_CODEC_FP16 else codes[p])
+        s = None if scales is None else _up(scales[p])
+        if counts[p] == 0:
+            W.nan_poison(c)
+            if s is not None:
+                W.nan_poison(s)
+        dc.append(c)
+        ds.append(s)
+    ga = D.dedloc_group_allreduce(dc, counts, m, L, codec, ds if scales is not None else None)
+    oc, osc, po = oracle.group_allreduce(codes, counts, m, codec, scales)
+    assert ga.n_out == oc.shape[0]
+    assert np.array_equal(ga.peer_out, po)
+    for g in range(ga.n_out):
+        if not np.any(po == g):
+            continue  # a group that produced nothing
+        if codec == D.DEDLOC_CODEC_FP16:
+            assert np.array_equal(_u16(ga.messages[g]), oc[g]), g
+        else:
+            assert np.array_equal(_i8(ga.messages[g]), oc[g]), g
+            assert np.array_equal(_bits(_np(ga.scales[g])), _bits(osc[g])), g
+
+
+def test_group_allreduce_full_size_xlarge():
+    """ALBERT-xlarge-sized messages (58.7M elements, 64 peers, int8) in
+    groups of 8: two iterations; sampled blocks of every output checked."""
+    wl = W.ALBERT_XLARGE
+    counts = W.sample_counts(wl)
+    L = wl.P
+    rng = np.random.default_rng(77)
+    blocks = sorted(set(int(b) for b in rng.integers(0, (L + 1023) // 1024, 6)) | {(L - 1) // 1024})
+    dc, ds, host = [], [], {b: [] for b in blocks}
+    for p in range(wl.n_peers):
+        g = W.peer_gradient(wl, p, DEV)
+        for b in blocks:
+            host[b].append(g[b * 1024:min((b + 1) * 1024, L)].cpu().numpy())
+        c, s = D.dedloc_encode(g, D.DEDLOC_CODEC_I8)
+        del g
+        if counts[p] == 0:
+            W.nan_poison(c)
+            W.nan_poison(s)
+        dc.append(c)
+        ds.append(s)
+    ga = D.dedloc_group_allreduce(dc, counts, 8, L, D.DEDLOC_CODEC_I8, ds)
+    torch.cuda.synchronize()
+    for b in blocks:
+        enc = [oracle.encode_i8(x, 1024) for x in host[b]]
+        oc, osc, po = oracle.group_allreduce([c for c, _ in enc], counts, 8, oracle.CODEC_I8, [s for _, s in enc])
+        assert np.array_equal(ga.peer_out, po)
+        n = host[b][0].size
+        for g in set(int(x) for x in po):
+            assert np.array_equal(_i8(ga.messages[g][b * 1024:b * 1024 + n]), oc[g]), (b, g)
+            assert _bits(_np(ga.scales[g][b:b + 1]))[0] == _bits(osc[g])[0], (b, g)
