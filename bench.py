@@ -32,6 +32,10 @@ def _parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="albert_large")
+    ap.add_argument("--mode", default="round", choices=["round", "group"],
+                    help="round: the averaging round (default); group: the group (Moshpit) "
+                         "all-reduce of the workload's peer messages")
+    ap.add_argument("--group-size", type=int, default=8)
     ap.add_argument("--optimizer", default="lamb", choices=["lamb", "lars"],
                     help="optimizer after the gather: LAMB (ALBERT runs) or LARS (SwAV runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -190,6 +194,70 @@ def measured_traffic(kernel, workload):
     return rec["hbm_bytes_per_launch"], os.path.relpath(path, root)
 
 
+def bench_group(args, wl):
+    """Group (Moshpit) all-reduce of the workload's peer messages in groups
+    of --group-size: ceil(log_m n) iterations, one launch each.  Algorithmic
+    bytes per iteration: every member's message read once (N_k * P * b) and
+    every group message written once (G_k * P * b)."""
+    import torch
+    from paper_2106_10207_amd import dedloc as D
+    from paper_2106_10207_amd import harness as H
+    from paper_2106_10207_amd import workloads as W
+    dr = H.DeviceRound(wl, "cuda")
+    m = args.group_size
+    ga = D.GroupAllreduce(dr.codes, dr.counts, m, wl.P, dr.codec,
+                          dr.scales if dr.codec == D.DEDLOC_CODEC_I8 else None)
+    # member and group counts per iteration from the same grid rule as the library
+    n = wl.n_peers
+    d = D.group_iterations(n, m)
+    cnt = list(dr.counts) + [0] * (m ** d - n)
+    reads = writes = 0
+    lo = 1
+    for k in range(d):
+        new = cnt[:]
+        for g in range(m ** d // m):
+            base = (g // lo) * lo * m + (g % lo)
+            members = [base + j * lo for j in range(m)]
+            tot = sum(cnt[s] for s in members)
+            reads += sum(1 for s in members if cnt[s] > 0)
+            writes += 1 if tot > 0 else 0
+            for s in members:
+                new[s] = tot
+        cnt = new
+        lo *= m
+    alg = (reads + writes) * wl.P * wl.wire_bytes_per_elem
+    for _ in range(args.warmup):
+        ga()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        ga()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    D.dedloc_profile_begin(64 * args.steps + 64)
+    for _ in range(args.steps):
+        ga()
+    prof = D.dedloc_profile_end()
+    kname = max(prof, key=lambda k: prof[k][0])
+    kms = prof[kname][0] / args.steps
+    peer_bytes = dr.bytes_peer_input()
+    return {
+        "metric": "group all-reduce GB/s of peer input",
+        "value": round(peer_bytes / (ms * 1e-3) / 1e9, 2),
+        "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "mode": "group", "group_size": m, "iterations": d,
+                   "peers": n, "wire": wl.codec},
+        "roofline": {"bound": "hbm", "kernel": kname, "achieved": round(alg / (kms * 1e-3) / 1e9, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(alg / (kms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "algorithmic_bytes_per_step": alg, "launches_per_step": prof[kname][1] / args.steps},
+    }
+
+
 def cpu_baseline(wl, dr, reps):
     """The oracle (plain sequential C) on the same workload: one local encode
     plus one round, on the host, timed after its inputs are prepared."""
@@ -272,6 +340,9 @@ def main():
     wl = W.WORKLOADS[args.workload]
     torch.cuda.set_device(0)
     D.load()
+    if args.mode == "group":
+        print(json.dumps(bench_group(args, wl)), flush=True)
+        return
     dr = H.DeviceRound(wl, "cuda", keep_local_grad=True, optimizer=args.optimizer)
     bw = W.bandwidth_weights(wl)
 

@@ -256,6 +256,22 @@ int dedloc_group_allreduce(const void *const *peer_codes, const float *const *pe
                            float *out_scales, uint32_t *peer_out, uint32_t *n_out, void *ws,
                            size_t ws_bytes, void *stream);
 
+/* Local accumulation (Section 3.1: every peer accumulates gradients at its
+ * own pace until the collaboration reaches the target batch).  A micro-batch
+ * of batch_samples samples whose mean gradient is grad (fp32, or fp16 codes
+ * with grad_codec = DEDLOC_CODEC_FP16) is added as
+ *     acc[e] = fma(batch_samples, grad[e], acc[e]).
+ * acc, grad: device, n elements, 16-byte aligned. */
+int dedloc_accumulate(float *acc, const void *grad, int32_t grad_codec, uint64_t n,
+                      float batch_samples, void *stream);
+
+/* The sender's message at the start of a round: the peer's mean gradient
+ * acc[e] / count (one correctly rounded division; count = samples
+ * accumulated, in [1, 2^24]) encoded as by dedloc_encode; reset != 0 zeroes
+ * acc afterwards for the next round.  count == 0 -> ZERO_WEIGHT. */
+int dedloc_finalize(float *acc, uint64_t n, uint32_t count, int32_t codec, uint32_t block,
+                    void *codes, float *scales, int32_t reset, void *stream);
+
 /* Per-kernel timing (tracing support for benchmarks).  Between
  * dedloc_profile_begin() and dedloc_profile_end() every kernel the library
  * enqueues is bracketed by a pair of HIP events on its stream; at most

@@ -15,6 +15,7 @@ Functions and the passages they follow:
   round      - Sections 3.1-3.2 (reduce-scatter, gather, one optimizer step)
   round_lars - the same round with the LARS step
   group_allreduce - Section 3.2 "Node failures" / Appendix C (group averaging)
+  accumulate/finalize - Section 3.1 (local accumulation to the target batch)
 """
 
 from __future__ import annotations
@@ -88,6 +89,8 @@ def _L():
         _lib.oracle_round_lars.argtypes = [vp, vp, vp, u32, vp, u32, ctypes.c_int, u32,
                                            vp, vp, vp, vp, u64, vp, vp, u32,
                                            ctypes.POINTER(_LarsCfg), vp, vp, vp]
+        _lib.oracle_accumulate.argtypes = [vp, vp, ctypes.c_int, sz, ctypes.c_float]
+        _lib.oracle_finalize.argtypes = [vp, sz, u32, ctypes.c_int, u32, vp, vp, ctypes.c_int, vp]
         _lib.oracle_group_allreduce.argtypes = [vp, vp, vp, u32, u32, sz, ctypes.c_int, u32, u32,
                                                 vp, vp, vp, vp, vp, vp, vp]
     return _lib
@@ -330,3 +333,28 @@ def group_allreduce(peer_codes, counts, m: int, codec: int, peer_scales=None, bl
                                      ctypes.byref(n_out), _p(work), _p(wsc) if nsc else None, _p(scratch))
     _check(rc)
     return out, (osc if nsc else None), peer_out
+
+
+def accumulate(acc, g, b: float):
+    """acc + b*g (fma per element); g fp32 or fp16 codes (uint16)."""
+    acc = _c(acc, np.float32).copy()
+    if g.dtype == np.uint16:
+        gc, code = _c(g, np.uint16), 1
+    else:
+        gc, code = _c(g, np.float32), 0
+    _L().oracle_accumulate(_p(acc), _p(gc), code, acc.size, b)
+    return acc
+
+
+def finalize(acc, count: int, codec: int, block: int = 1024, reset: bool = True):
+    """Encode acc / count; returns (codes, scales or None, acc after)."""
+    acc = _c(acc, np.float32).copy()
+    n = acc.size
+    if codec == CODEC_FP16:
+        codes, scales = np.empty(n, np.uint16), None
+    else:
+        codes, scales = np.empty(n, np.int8), np.empty((n + block - 1) // block, np.float32)
+    scratch = np.empty(max(n, 1), np.float32)
+    _check(_L().oracle_finalize(_p(acc), n, count, codec, block, _p(codes), _p(scales), int(reset),
+                                _p(scratch)))
+    return codes, scales, acc

@@ -498,3 +498,32 @@ int oracle_group_allreduce(const void *const *peer_codes, const float *const *pe
     *n_out = groups;
     return OR_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Local accumulation (Section 3.1: each peer accumulates gradients at its
+ * own pace until the collaboration reaches the target batch).  A micro-batch
+ * of b samples whose mean gradient is g adds b*g to the running sum:
+ *     acc = fmaf(b, g, acc)          (one rounding per element per batch)
+ * When the round starts the peer's mean gradient is acc / count (one
+ * correctly rounded division, count = samples accumulated), encoded with the
+ * wire codec; reset != 0 then zeroes acc for the next round.  g is fp32
+ * (codec 0) or fp16 codes (codec 1). */
+void oracle_accumulate(float *acc, const void *g, int g_codec, size_t n, float b)
+{
+    for (size_t i = 0; i < n; i++) {
+        float gi = g_codec == 0 ? ((const float *)g)[i] : f16_to_f32(((const uint16_t *)g)[i]);
+        acc[i] = fmaf(b, gi, acc[i]);
+    }
+}
+
+int oracle_finalize(float *acc, size_t n, uint32_t count, int codec, uint32_t block,
+                    void *codes, float *scales, int reset, float *scratch)
+{
+    if (count == 0 || count > (1u << 24)) return count == 0 ? OR_EZERO : OR_EINVAL;
+    float c = (float)count;
+    for (size_t i = 0; i < n; i++) scratch[i] = acc[i] / c;
+    encode_any(codec, scratch, n, codec == 1 ? 1 : block, codes, scales);
+    if (reset)
+        for (size_t i = 0; i < n; i++) acc[i] = 0.0f;
+    return OR_OK;
+}

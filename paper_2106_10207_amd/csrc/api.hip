@@ -41,13 +41,13 @@ enum Kind {
     K_ENCODE_FP16, K_DECODE_FP16, K_ENCODE_I8, K_DECODE_I8, K_REDUCE_FP16, K_REDUCE_I8,
     K_LAMB_A_F32, K_LAMB_A_FP16, K_LAMB_A_I8, K_LAMB_A_FUSED_FP16, K_LAMB_TRUST, K_LAMB_B,
     K_LARS_A_F32, K_LARS_A_FP16, K_LARS_A_I8, K_LARS_A_FUSED_FP16, K_LARS_TRUST, K_LARS_B,
-    K_FILL, K_COUNT
+    K_ACCUMULATE, K_FINALIZE_FP16, K_FINALIZE_I8, K_FILL, K_COUNT
 };
 const char *const kKindNames[K_COUNT] = {
     "encode_fp16", "decode_fp16", "encode_i8", "decode_i8", "reduce_fp16", "reduce_i8",
     "lamb_a_f32", "lamb_a_fp16", "lamb_a_i8", "lamb_a_fused_fp16", "lamb_trust", "lamb_b",
     "lars_a_f32", "lars_a_fp16", "lars_a_i8", "lars_a_fused_fp16", "lars_trust", "lars_b",
-    "fill_zero"};
+    "accumulate", "finalize_fp16", "finalize_i8", "fill_zero"};
 
 struct Profiler {
     std::mutex mu;
@@ -666,6 +666,42 @@ int dedloc_group_allreduce(const void *const *peer_codes, const float *const *pe
     for (uint32_t i = 0; i < n_peers; i++) peer_out[i] = src[i] >= 0 ? (uint32_t)src[i] : 0xffffffffu;
     *n_out = gp.groups;
     return DEDLOC_OK;
+}
+
+int dedloc_accumulate(float *acc, const void *grad, int32_t grad_codec, uint64_t n, float batch_samples,
+                      void *stream) {
+    if (grad_codec != DEDLOC_CODEC_F32 && grad_codec != DEDLOC_CODEC_FP16)
+        return fail(DEDLOC_ERR_INVALID_ARG, "accumulate takes fp32 or fp16 gradients");
+    if (n == 0) return DEDLOC_OK;
+    if (!acc || !grad) return fail(DEDLOC_ERR_INVALID_ARG, "acc and grad must not be NULL");
+    if (!aligned(acc, 16) || !aligned(grad, 16)) return fail(DEDLOC_ERR_ALIGN, "acc and grad must be 16-byte aligned");
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = timed(K_ACCUMULATE, s, [&] {
+        return launch_accumulate(acc, grad, grad_codec == DEDLOC_CODEC_FP16, n, batch_samples, s);
+    });
+    return e == hipSuccess ? DEDLOC_OK : hip_fail(e, "accumulate launch");
+}
+
+int dedloc_finalize(float *acc, uint64_t n, uint32_t count, int32_t codec, uint32_t block, void *codes,
+                    float *scales, int32_t reset, void *stream) {
+    int rc = check_codec(codec, block, false);
+    if (rc) return rc;
+    if (count == 0) return fail(DEDLOC_ERR_ZERO_WEIGHT, "no samples were accumulated");
+    if (count > (1u << 24)) return fail(DEDLOC_ERR_INVALID_ARG, "count %u exceeds 2^24", count);
+    if (n == 0) return DEDLOC_OK;
+    if (!acc || !codes) return fail(DEDLOC_ERR_INVALID_ARG, "acc and codes must not be NULL");
+    if (!aligned(acc, 16) || !aligned(codes, 16)) return fail(DEDLOC_ERR_ALIGN, "acc and codes must be 16-byte aligned");
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e;
+    if (codec == DEDLOC_CODEC_FP16) {
+        e = timed(K_FINALIZE_FP16, s, [&] { return launch_finalize_fp16(acc, n, (float)count, (uint16_t *)codes, reset, s); });
+    } else {
+        if (!scales || !aligned(scales, 4)) return fail(DEDLOC_ERR_INVALID_ARG, "int8 finalize needs aligned scales");
+        e = timed(K_FINALIZE_I8, s, [&] {
+            return launch_finalize_i8(acc, n, (float)count, (int8_t *)codes, scales, reset, s);
+        });
+    }
+    return e == hipSuccess ? DEDLOC_OK : hip_fail(e, "finalize launch");
 }
 
 int dedloc_profile_begin(uint32_t max_launches) {

@@ -121,6 +121,10 @@ hipError_t launch_opt_trust(int opt, const Chunk &ch, const OptParams &op, const
 hipError_t launch_opt_b(int opt, int src, const Chunk &ch, uint32_t n_tiles, const GradArgs &ga,
                         const OptParams &op, float *x, float *m, float *v, const LambWs &ws,
                         hipStream_t s);
+hipError_t launch_accumulate(float *acc, const void *grad, bool fp16, uint64_t n, float b, hipStream_t s);
+hipError_t launch_finalize_fp16(float *acc, uint64_t n, float count, uint16_t *codes, int reset, hipStream_t s);
+hipError_t launch_finalize_i8(float *acc, uint64_t n, float count, int8_t *codes, float *scales, int reset,
+                              hipStream_t s);
 hipError_t launch_fill_zero(void *p, size_t bytes, hipStream_t s);
 
 }  // namespace dedloc

@@ -551,6 +551,82 @@ __global__ __launch_bounds__(kWG) void opt_b_kernel(const Chunk ch, const GradAr
     }
 }
 
+// ------------------------------------------------ local accumulation
+// acc = fma(b, g, acc): a micro-batch of b samples with mean gradient g.
+template <bool G16>
+__global__ __launch_bounds__(kWG) void accumulate_kernel(float *__restrict__ acc, const void *__restrict__ grad,
+                                                         uint64_t n, float b) {
+    const uint64_t e0 = ((uint64_t)blockIdx.x * kWG + threadIdx.x) * kVec;
+    if (e0 >= n) return;
+    const int cnt = (int)(n - e0 < (uint64_t)kVec ? n - e0 : (uint64_t)kVec);
+    float a[8], g[8];
+    load8(acc, e0, cnt, a);
+    if (G16) {
+        if (cnt == kVec) {
+            unpack_fp16x8(ld_stream((const u32x4 *)((const uint16_t *)grad + e0)), g);
+        } else {
+            for (int j = 0; j < kVec; j++) g[j] = j < cnt ? h2f(((const uint16_t *)grad)[e0 + j]) : 0.0f;
+        }
+    } else {
+        if (cnt == kVec) {
+            const f32x4 p = ld_stream((const f32x4 *)((const float *)grad + e0));
+            const f32x4 q = ld_stream((const f32x4 *)((const float *)grad + e0 + 4));
+            g[0] = p[0]; g[1] = p[1]; g[2] = p[2]; g[3] = p[3];
+            g[4] = q[0]; g[5] = q[1]; g[6] = q[2]; g[7] = q[3];
+        } else {
+            for (int j = 0; j < kVec; j++) g[j] = j < cnt ? ((const float *)grad)[e0 + j] : 0.0f;
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < 8; j++) a[j] = fmaf(b, g[j], a[j]);
+    store8(acc, e0, cnt, a);
+}
+
+// mean = acc / count, encoded fp16; acc zeroed when reset.
+__global__ __launch_bounds__(kWG) void finalize_fp16_kernel(float *__restrict__ acc, uint64_t n, float count,
+                                                            uint16_t *__restrict__ codes, int reset) {
+    const uint64_t e0 = ((uint64_t)blockIdx.x * kWG + threadIdx.x) * kVec;
+    if (e0 >= n) return;
+    const int cnt = (int)(n - e0 < (uint64_t)kVec ? n - e0 : (uint64_t)kVec);
+    float a[8];
+    load8(acc, e0, cnt, a);
+#pragma unroll
+    for (int j = 0; j < 8; j++) a[j] = a[j] / count;
+    if (cnt == kVec) {
+        st_stream((u32x4 *)(codes + e0), pack_fp16x8(a));
+    } else {
+        for (int j = 0; j < cnt; j++) codes[e0 + j] = (uint16_t)f2h(a[j]);
+    }
+    if (reset) {
+        const float z[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        store8(acc, e0, cnt, z);
+    }
+}
+
+// int8: one wave per 1024-element block, 16 elements per lane.
+__global__ __launch_bounds__(kWG) void finalize_i8_kernel(float *__restrict__ acc, uint64_t n, float count,
+                                                          int8_t *__restrict__ codes, float *__restrict__ scales,
+                                                          int reset) {
+    const uint64_t blk = (uint64_t)blockIdx.x * (kWG / 64) + (threadIdx.x >> 6);
+    if (blk * kI8Block >= n) return;  // whole wave past the end
+    const uint64_t e0 = blk * kI8Block + (threadIdx.x & 63) * kI8PerLane;
+    float val[kI8PerLane];
+#pragma unroll
+    for (int j = 0; j < kI8PerLane; j++) val[j] = (e0 + j < n) ? acc[e0 + j] / count : 0.0f;
+    float s;
+    const u32x4 c = encode_i8_wave(val, s);
+    if (e0 + kI8PerLane <= n) {
+        *(u32x4 *)(codes + e0) = c;
+    } else {
+        for (int j = 0; j < kI8PerLane; j++)
+            if (e0 + j < n) codes[e0 + j] = (int8_t)(c[j >> 2] >> (8 * (j & 3)));
+    }
+    if ((threadIdx.x & 63) == 0) scales[blk] = s;
+    if (reset)
+        for (int j = 0; j < kI8PerLane; j++)
+            if (e0 + j < n) acc[e0 + j] = 0.0f;
+}
+
 __global__ __launch_bounds__(kWG) void fill_zero_kernel(uint32_t *p, uint64_t n_words) {
     const uint64_t i = (uint64_t)blockIdx.x * kWG + threadIdx.x;
     if (i < n_words) p[i] = 0u;
@@ -637,6 +713,21 @@ hipError_t launch_opt_b(int opt, int src, const Chunk &ch, uint32_t n_tiles, con
     case kSrcI8: DEDLOC_LAUNCH(dim3(n_tiles), (opt_b_kernel<kSrcI8, kOptLars>), s, ch, ga, op, x, m, v, ws);
     default: return hipErrorInvalidValue;
     }
+}
+
+hipError_t launch_accumulate(float *acc, const void *grad, bool fp16, uint64_t n, float b, hipStream_t s) {
+    if (fp16) DEDLOC_LAUNCH(dim3(grid_for(n, (uint64_t)kWG * kVec)), accumulate_kernel<true>, s, acc, grad, n, b);
+    DEDLOC_LAUNCH(dim3(grid_for(n, (uint64_t)kWG * kVec)), accumulate_kernel<false>, s, acc, grad, n, b);
+}
+
+hipError_t launch_finalize_fp16(float *acc, uint64_t n, float count, uint16_t *codes, int reset, hipStream_t s) {
+    DEDLOC_LAUNCH(dim3(grid_for(n, (uint64_t)kWG * kVec)), finalize_fp16_kernel, s, acc, n, count, codes, reset);
+}
+
+hipError_t launch_finalize_i8(float *acc, uint64_t n, float count, int8_t *codes, float *scales, int reset,
+                              hipStream_t s) {
+    DEDLOC_LAUNCH(dim3(grid_for(n, (uint64_t)kI8Block * (kWG / 64))), finalize_i8_kernel, s, acc, n, count, codes,
+                  scales, reset);
 }
 
 hipError_t launch_fill_zero(void *p, size_t bytes, hipStream_t s) {

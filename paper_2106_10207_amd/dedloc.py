@@ -108,6 +108,10 @@ _SIGS = {
                                 ctypes.c_uint64, ctypes.c_int32, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p,
                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p],
                                ctypes.c_int),
+    "dedloc_accumulate": ([ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint64, ctypes.c_float,
+                           ctypes.c_void_p], ctypes.c_int),
+    "dedloc_finalize": ([ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int32, ctypes.c_uint32,
+                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p], ctypes.c_int),
     "dedloc_profile_begin": ([ctypes.c_uint32], ctypes.c_int),
     "dedloc_profile_end": ([ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "dedloc_kernel_kinds": ([], ctypes.c_int),
@@ -424,3 +428,23 @@ def dedloc_group_allreduce(peer_codes, counts, group_size: int, length: int, cod
                            block: int = DEDLOC_I8_BLOCK, stream=None) -> GroupAllreduce:
     dev = next(t.device for t in peer_codes if t is not None)
     return GroupAllreduce(peer_codes, counts, group_size, length, codec, peer_scales, block, dev)(stream)
+
+
+def dedloc_accumulate(acc, grad, batch_samples: float, stream=None):
+    """acc += batch_samples * grad (fp32 grad, or fp16 codes as int16)."""
+    import torch
+    codec = DEDLOC_CODEC_FP16 if grad.dtype in (torch.int16, torch.float16) else DEDLOC_CODEC_F32
+    _check(load().dedloc_accumulate(_dev(acc), _dev(grad), codec, acc.numel(), batch_samples, _stream(stream)))
+
+
+def dedloc_finalize(acc, count: int, codec: int, block: int = DEDLOC_I8_BLOCK, codes=None, scales=None,
+                    reset: bool = True, stream=None):
+    import torch
+    n = acc.numel()
+    if codes is None:
+        codes = torch.empty(n, dtype=torch.int16 if codec == DEDLOC_CODEC_FP16 else torch.int8, device=acc.device)
+    if scales is None and codec == DEDLOC_CODEC_I8:
+        scales = torch.empty((n + block - 1) // block, dtype=torch.float32, device=acc.device)
+    _check(load().dedloc_finalize(_dev(acc), n, count, codec, block, _dev(codes), _dev(scales), int(reset),
+                                  _stream(stream)))
+    return codes, scales

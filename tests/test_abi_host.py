@@ -189,3 +189,32 @@ def test_workspace_rejects_huge_tensor():
     off = np.array([0, 1 << 32], np.uint64)
     with pytest.raises(D.DedlocError):
         D.dedloc_lamb_workspace_bytes(1 << 32, off)
+
+
+def test_accumulate_finalize_validation():
+    lib = D.load()
+    A = 1 << 20
+    assert lib.dedloc_accumulate(A, A, 7, 64, 1.0, None) == D.DEDLOC_ERR_INVALID_ARG      # codec
+    assert lib.dedloc_accumulate(A + 4, A, 0, 64, 1.0, None) == D.DEDLOC_ERR_ALIGN
+    assert lib.dedloc_accumulate(A, A, 0, 0, 1.0, None) == D.DEDLOC_OK                    # empty
+    assert lib.dedloc_finalize(A, 64, 0, 1, 0, A, None, 1, None) == D.DEDLOC_ERR_ZERO_WEIGHT
+    assert lib.dedloc_finalize(A, 64, (1 << 24) + 1, 1, 0, A, None, 1, None) == D.DEDLOC_ERR_INVALID_ARG
+    assert lib.dedloc_finalize(A, 64, 5, 2, 1024, A, None, 1, None) == D.DEDLOC_ERR_INVALID_ARG  # no scales
+    assert lib.dedloc_finalize(A, 64, 5, 1, 0, A + 2, None, 1, None) == D.DEDLOC_ERR_ALIGN
+
+
+def test_group_allreduce_validation():
+    lib = D.load()
+    A = 1 << 20
+    pc = (ctypes.c_void_p * 3)(A, A, A)
+    cnt = np.array([1, 2, 3], np.uint32)
+    po = np.zeros(3, np.uint32)
+    nout = ctypes.c_uint32(0)
+    call = lambda m, ws=A, wsb=1 << 30, out=A: lib.dedloc_group_allreduce(
+        pc, None, cnt.ctypes.data, 3, m, 64, D.DEDLOC_CODEC_FP16, 0, out, None, po.ctypes.data,
+        ctypes.byref(nout), ws, wsb, None)
+    assert call(1) == D.DEDLOC_ERR_INVALID_ARG             # group size < 2
+    assert call(2, out=A + 16) == D.DEDLOC_ERR_ALIGN       # outputs on 256-byte boundaries
+    assert call(2, wsb=0) == D.DEDLOC_ERR_WORKSPACE
+    assert lib.dedloc_group_allreduce_workspace_bytes(3, 2, 64, D.DEDLOC_CODEC_FP16, 0) == 2 * 2 * 256
+    assert lib.dedloc_group_allreduce_workspace_bytes(65, 2, 64, D.DEDLOC_CODEC_FP16, 0) == 0
