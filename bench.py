@@ -32,9 +32,10 @@ def _parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="albert_large")
-    ap.add_argument("--mode", default="round", choices=["round", "group"],
+    ap.add_argument("--mode", default="round", choices=["round", "group", "balance"],
                     help="round: the averaging round (default); group: the group (Moshpit) "
-                         "all-reduce of the workload's peer messages")
+                         "all-reduce of the workload's peer messages; balance: host solve time of "
+                         "the load-balancing LP for 4..32 peers")
     ap.add_argument("--group-size", type=int, default=8)
     ap.add_argument("--optimizer", default="lamb", choices=["lamb", "lars"],
                     help="optimizer after the gather: LAMB (ALBERT runs) or LARS (SwAV runs)")
@@ -194,6 +195,30 @@ def measured_traffic(kernel, workload):
     return rec["hbm_bytes_per_launch"], os.path.relpath(path, root)
 
 
+def bench_balance():
+    """Host time of dedloc_balance (the library's simplex) and of the oracle
+    (HiGHS on the literal n^3-constraint program) on random collaborations:
+    compute 1..200 samples/s, bandwidths 10..1000 Mbit/s, ALBERT-large P."""
+    from oracle import lp
+    from paper_2106_10207_amd import dedloc as D
+    rows = []
+    for n in (4, 8, 16, 24, 32):
+        rng = np.random.default_rng(n)
+        s = rng.uniform(1, 200, n)
+        d = rng.uniform(10, 1000, n) * 1e5 / 4
+        u = rng.uniform(10, 1000, n) * 1e5 / 4
+        B, P = 4096.0, 17_683_968.0
+        t0 = time.perf_counter()
+        r = D.dedloc_balance(s, d, u, B, P)
+        t1 = time.perf_counter()
+        o = lp.solve(s, d, u, B, P)
+        t2 = time.perf_counter()
+        rows.append({"peers": n, "lib_ms": round((t1 - t0) * 1e3, 2), "oracle_ms": round((t2 - t1) * 1e3, 1),
+                     "xi": r["xi"], "xi_oracle": o["xi"]})
+    return {"metric": "load-balancing LP solve time (host)", "unit": "ms", "higher_is_better": False,
+            "cores": 1, "rows": rows}
+
+
 def bench_group(args, wl):
     """Group (Moshpit) all-reduce of the workload's peer messages in groups
     of --group-size: ceil(log_m n) iterations, one launch each.  Algorithmic
@@ -322,6 +347,10 @@ def main():
     from paper_2106_10207_amd import dedloc as D
     from paper_2106_10207_amd import harness as H
     from paper_2106_10207_amd import workloads as W
+
+    if args.mode == "balance":
+        print(json.dumps(bench_balance()), flush=True)
+        return
 
     if args.summarize_counters:
         for f in summarize_counters(args.summarize_counters, args.workload):

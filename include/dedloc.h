@@ -272,6 +272,35 @@ int dedloc_accumulate(float *acc, const void *grad, int32_t grad_codec, uint64_t
 int dedloc_finalize(float *acc, uint64_t n, uint32_t count, int32_t codec, uint32_t block,
                     void *codes, float *scales, int32_t reset, void *stream);
 
+/* Load balancer (Section 3.2, Appendix B): the relaxed linear program
+ * (Eq. main_problem_appendix_relaxed) that maximises training steps per
+ * second xi over the send rates a_ij (peer i -> reducer j), the return rates
+ * g_ij (reducer i -> peer j) and the compute indicators c_i in [0, 1]:
+ *   xi <= sum_i s_i c_i / B;   xi <= sum_j g_ji / P            (every i)
+ *   g_ij <= a_ki + (1 - c_k) d_i                               (every i, j, k)
+ *   sum_{j != i} (a_ji + g_ji) <= d_i;  sum_{j != i} (a_ij + g_ij) <= u_i
+ *   a_ij + g_ij <= t_ij (where finite);  a, g >= 0;  0 <= c <= 1
+ * solved on the host by a deterministic dense simplex (the n^3 aggregation
+ * constraints are replaced by an exactly equivalent O(n^2) set with a rate
+ * variable per reducer).  Reducer i's share is proportional to min_{j != i}
+ * g_ij (the appendix's "fraction" equation; the rate to itself is free).
+ * Units: s in samples/s, d, u, t in parameters/s, B samples, P parameters.
+ * Peers with can_aggregate[i] == 0 receive nothing to aggregate (a_ji = g_ij
+ * = 0).  All arrays are host memory; t (n*n, row-major, INFINITY = no limit)
+ * and can_aggregate may be NULL.
+ * Outputs: xi, c[n], frac[n] (sums to 1), weights[n] (nullable): frac scaled
+ * to integers summing to about 2^24, ready for dedloc_partition; a[n*n] and
+ * g[n*n] (nullable) in parameters/s.  n <= DEDLOC_BALANCE_MAX_PEERS. */
+#define DEDLOC_BALANCE_MAX_PEERS 32
+typedef struct {
+    uint32_t n;
+    const double *s, *d, *u, *t;
+    const uint8_t *can_aggregate;
+    double B, P;
+} dedloc_balance_problem;
+int dedloc_balance(const dedloc_balance_problem *pr, double *xi, double *c, double *frac,
+                   uint64_t *weights, double *a, double *g);
+
 /* Per-kernel timing (tracing support for benchmarks).  Between
  * dedloc_profile_begin() and dedloc_profile_end() every kernel the library
  * enqueues is bracketed by a pair of HIP events on its stream; at most

@@ -39,12 +39,23 @@ def _idx(n):
 def solve(s, d, u, B, P, t=None, can_aggregate=None, fix_c=None):
     """Solve the relaxed LP.  Returns dict(xi, a, g, c, frac, status).
 
-    fix_c: optional array; where not NaN, c_i is fixed to that value."""
+    fix_c: optional array; where not NaN, c_i is fixed to that value.
+
+    Rates are handed to the solver in whole vectors per second (bandwidths
+    divided by P, and P = 1): the same program in other units.  Left in
+    parameters per second, the 1/P coefficients sit nine orders of magnitude
+    below the bandwidths and HiGHS stops within its tolerances but measurably
+    short of the optimum."""
     import scipy.optimize as so
     import scipy.sparse as sp
 
     s, d, u = (np.asarray(v, dtype=np.float64) for v in (s, d, u))
     n = s.size
+    d, u = d / P, u / P
+    if t is not None:
+        t = np.asarray(t, dtype=np.float64) / P
+    Pu = P
+    P = 1.0
     a, g, c, xi, nv = _idx(n)
     rows, cols, vals, rhs = [], [], [], []
     r = 0
@@ -92,8 +103,8 @@ def solve(s, d, u, B, P, t=None, can_aggregate=None, fix_c=None):
     if res.status != 0:
         return dict(status=res.status, xi=None)
     x = res.x
-    A_ = x[:n * n].reshape(n, n)
-    G = x[n * n:2 * n * n].reshape(n, n)
+    A_ = x[:n * n].reshape(n, n) * Pu
+    G = x[n * n:2 * n * n].reshape(n, n) * Pu
     C = x[2 * n * n:2 * n * n + n]
     return dict(status=0, xi=float(x[xi]), a=A_, g=G, c=C, frac=shares(G))
 

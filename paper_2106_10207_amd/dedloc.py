@@ -67,6 +67,12 @@ def lars_cfg(lr=4.8, momentum=0.9, trust_coef=1e-3, weight_decay=1e-6,
     return dedloc_lars_cfg(lr, momentum, trust_coef, weight_decay, int(force_unit_trust))
 
 
+class dedloc_balance_problem(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_uint32), ("s", ctypes.c_void_p), ("d", ctypes.c_void_p),
+                ("u", ctypes.c_void_p), ("t", ctypes.c_void_p), ("can_aggregate", ctypes.c_void_p),
+                ("B", ctypes.c_double), ("P", ctypes.c_double)]
+
+
 _lib = None
 
 _SIGS = {
@@ -112,6 +118,8 @@ _SIGS = {
                            ctypes.c_void_p], ctypes.c_int),
     "dedloc_finalize": ([ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_int32, ctypes.c_uint32,
                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p], ctypes.c_int),
+    "dedloc_balance": ([ctypes.POINTER(dedloc_balance_problem), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "dedloc_profile_begin": ([ctypes.c_uint32], ctypes.c_int),
     "dedloc_profile_end": ([ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "dedloc_kernel_kinds": ([], ctypes.c_int),
@@ -448,3 +456,23 @@ def dedloc_finalize(acc, count: int, codec: int, block: int = DEDLOC_I8_BLOCK, c
     _check(load().dedloc_finalize(_dev(acc), n, count, codec, block, _dev(codes), _dev(scales), int(reset),
                                   _stream(stream)))
     return codes, scales
+
+
+def dedloc_balance(s, d, u, B: float, P: float, t=None, can_aggregate=None):
+    """Solve the load-balancing LP on the host.  Returns dict(xi, c, frac,
+    weights, a, g) (rates in parameters/s)."""
+    s, d, u = (_host(v, np.float64) for v in (s, d, u))
+    n = s.size
+    tt = None if t is None else _host(t, np.float64).reshape(n * n)
+    ca = None if can_aggregate is None else _host(can_aggregate, np.uint8)
+    pr = dedloc_balance_problem(n, _ptr(s), _ptr(d), _ptr(u), _ptr(tt), _ptr(ca), B, P)
+    xi = ctypes.c_double(0.0)
+    c = np.zeros(n)
+    frac = np.zeros(n)
+    w = np.zeros(n, np.uint64)
+    a = np.zeros(n * n)
+    g = np.zeros(n * n)
+    rc = load().dedloc_balance(ctypes.byref(pr), ctypes.byref(xi), _ptr(c), _ptr(frac), _ptr(w), _ptr(a), _ptr(g))
+    if rc != DEDLOC_OK:
+        raise DedlocError(rc, "load-balancing LP failed (invalid problem or no convergence)")
+    return dict(xi=xi.value, c=c, frac=frac, weights=w, a=a.reshape(n, n), g=g.reshape(n, n))

@@ -1,0 +1,95 @@
+"""The library's load balancer (dedloc_balance, host C++ simplex) against the
+oracle's LP (Appendix B's program written out literally, solved by HiGHS).
+
+The optimum xi is unique and must agree; optimal points need not be unique,
+so the library's own (a, g, c) is checked for feasibility in the original
+n^3-constraint program, and its shares are recomputed from its g."""
+
+import numpy as np
+import pytest
+
+from oracle import lp
+from paper_2106_10207_amd import dedloc as D
+
+
+def _problem(n, seed, regional=False, aux=False):
+    rng = np.random.default_rng(seed)
+    s = rng.uniform(1, 200, n)
+    if aux:
+        s[rng.choice(n, max(1, n // 4), replace=False)] = 0.0  # peers without GPUs
+    d = rng.uniform(10, 1000, n) * 1e5 / 4          # Mbit/s -> fp32 parameters/s
+    u = rng.uniform(10, 1000, n) * 1e5 / 4
+    t = None
+    if regional:
+        t = np.full((n, n), np.inf)
+        for _ in range(n):
+            i, j = rng.integers(0, n, 2)
+            t[i, j] = rng.uniform(1, 50) * 1e5 / 4
+    return s, d, u, t
+
+
+def _check(r, s, d, u, B, P, t=None, agg=None):
+    o = lp.solve(s, d, u, B, P, t=t, can_aggregate=agg)
+    assert np.isclose(r["xi"], o["xi"], rtol=1e-9, atol=0), (r["xi"], o["xi"])
+    sol = dict(a=r["a"], g=r["g"], c=r["c"], xi=r["xi"])
+    assert lp.violation(sol, s, d, u, B, P, t=t, can_aggregate=agg) < 1e-9
+    assert np.all(r["c"] >= -1e-12) and np.all(r["c"] <= 1 + 1e-12)
+    assert np.all(r["frac"] >= 0) and np.isclose(r["frac"].sum(), 1.0)
+    assert np.allclose(r["frac"], lp.shares(r["g"]) if agg is None else r["frac"], rtol=1e-9, atol=1e-12)
+    assert abs(int(r["weights"].sum()) - (1 << 24)) <= len(s)
+    return o
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 8, 12, 16])
+@pytest.mark.parametrize("variant", ["plain", "aux", "regional"])
+def test_matches_oracle(n, variant):
+    s, d, u, t = _problem(n, 1000 * n + len(variant), regional=variant == "regional", aux=variant == "aux")
+    B, P = 4096.0, 17_683_968.0
+    r = D.dedloc_balance(s, d, u, B, P, t=t)
+    _check(r, s, d, u, B, P, t=t)
+
+
+def test_non_aggregators():
+    n = 6
+    s, d, u, _ = _problem(n, 7)
+    agg = np.array([1, 0, 1, 1, 0, 1], np.uint8)
+    r = D.dedloc_balance(s, d, u, 4096.0, 2.5e7, can_aggregate=agg)
+    _check(r, s, d, u, 4096.0, 2.5e7, agg=agg.astype(bool))
+    assert r["frac"][1] == 0 and r["frac"][4] == 0
+    assert np.all(r["a"][:, 1] == 0) and np.all(r["g"][4, :] == 0)
+
+
+def test_closed_forms():
+    n = 5
+    big = np.full(n, 1e15)
+    r = D.dedloc_balance(np.full(n, 100.0), big, big, 4096.0, 1e6)          # compute-bound
+    assert np.isclose(r["xi"], n * 100.0 / 4096.0, rtol=1e-12)
+    b = np.full(n, 1e6)
+    r = D.dedloc_balance(np.full(n, 1e12), b, b, 1.0, 2e6)                   # relaxation bound 2b/P
+    assert np.isclose(r["xi"], 2 * 1e6 / 2e6, rtol=1e-12)
+
+
+def test_deterministic_and_partition():
+    s, d, u, _ = _problem(10, 3)
+    r1 = D.dedloc_balance(s, d, u, 4096.0, 2.5e7)
+    r2 = D.dedloc_balance(s, d, u, 4096.0, 2.5e7)
+    for k in ("xi", "c", "frac", "weights", "a", "g"):
+        assert np.array_equal(np.asarray(r1[k]), np.asarray(r2[k])), k
+    P = 25_557_032
+    bounds = D.dedloc_partition(P, 10, r1["weights"], 64)
+    sizes = np.diff(bounds.astype(np.int64))
+    assert bounds[-1] == P and np.all(sizes >= 0)
+    assert np.all(np.abs(sizes - r1["frac"] * P) <= 64 + P * 1e-6)
+
+
+@pytest.mark.parametrize("bad", ["n0", "n33", "B", "neg"])
+def test_rejects(bad):
+    n = 33 if bad == "n33" else 3
+    s, d, u = np.ones(n), np.ones(n), np.ones(n)
+    B = 0.0 if bad == "B" else 1.0
+    if bad == "neg":
+        d[1] = -1.0
+    if bad == "n0":
+        s, d, u = np.ones(0), np.ones(0), np.ones(0)
+    with pytest.raises(D.DedlocError):
+        D.dedloc_balance(s, d, u, B, 1.0)
