@@ -37,6 +37,8 @@ def _parse():
                          "all-reduce of the workload's peer messages; balance: host solve time of "
                          "the load-balancing LP for 4..32 peers")
     ap.add_argument("--group-size", type=int, default=8)
+    ap.add_argument("--graph", action="store_true",
+                    help="capture one step (encode + round) in a HIP graph and time its replays")
     ap.add_argument("--optimizer", default="lamb", choices=["lamb", "lars"],
                     help="optimizer after the gather: LAMB (ALBERT runs) or LARS (SwAV runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -375,10 +377,25 @@ def main():
     dr = H.DeviceRound(wl, "cuda", keep_local_grad=True, optimizer=args.optimizer)
     bw = W.bandwidth_weights(wl)
 
-    def step():
+    def eager_step():
         D.dedloc_partition(wl.P, wl.n_shards, bw, wl.shard_align)
         dr.encode_local()
         dr.run()
+
+    step = eager_step
+    if args.graph:
+        # the partition is host-only integer work, outside the graph
+        side = torch.cuda.Stream()
+        graph = torch.cuda.CUDAGraph()
+        eager_step()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=side):
+            dr.encode_local()
+            dr.call(stream=side)
+
+        def step():
+            D.dedloc_partition(wl.P, wl.n_shards, bw, wl.shard_align)
+            graph.replay()
 
     for _ in range(args.warmup):
         step()
@@ -399,7 +416,7 @@ def main():
     # same K steps again with per-kernel events (roofline of the dominant kernel)
     D.dedloc_profile_begin(64 * args.steps + 64)
     for _ in range(args.steps):
-        step()
+        eager_step()
     prof = D.dedloc_profile_end()
     kname, roof, per_kernel = kernel_roofline(dr, prof, args.steps)
     roof["traffic"], roof["traffic_source"] = measured_traffic(kname, wl.name)
@@ -447,6 +464,7 @@ def main():
             "wire": wl.codec,
             "shards": wl.n_shards,
             "optimizer": args.optimizer,
+            "graph": bool(args.graph),
             "parallelism": "single GPU; peers are HBM regions",
         },
         "params_per_s": round(wl.P / t, 1),

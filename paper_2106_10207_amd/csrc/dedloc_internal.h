@@ -20,6 +20,12 @@ namespace dedloc {
 #ifndef DEDLOC_NT_STORES
 #define DEDLOC_NT_STORES 0    // non-temporal hint on streamed stores
 #endif
+#ifndef DEDLOC_NT_MSG_STORES
+#define DEDLOC_NT_MSG_STORES 1  // non-temporal hint on stores of encoded messages
+#endif
+#ifndef DEDLOC_TRUST_UNROLL
+#define DEDLOC_TRUST_UNROLL 8   // tile partials loaded per lane before summing
+#endif
 #ifndef DEDLOC_B_REVERSE
 #define DEDLOC_B_REVERSE 1    // pass B visits tiles last-to-first (its re-reads
                               // start with what pass A touched last)

@@ -27,6 +27,12 @@ __device__ __forceinline__ void st_stream(T *p, T v) {
     if (DEDLOC_NT_STORES) __builtin_nontemporal_store(v, p);
     else *p = v;
 }
+// Stores of encoded messages (read by other peers, not by this kernel).
+template <typename T>
+__device__ __forceinline__ void st_msg(T *p, T v) {
+    if (DEDLOC_NT_MSG_STORES) __builtin_nontemporal_store(v, p);
+    else *p = v;
+}
 
 __device__ __forceinline__ float h2f(unsigned bits) {
     return (float)__builtin_bit_cast(_Float16, (uint16_t)bits);
@@ -115,7 +121,7 @@ __global__ __launch_bounds__(kWG) void encode_fp16_kernel(const float *__restric
     if (e0 + kVec <= n) {
         const f32x4 a = ld_stream((const f32x4 *)(x + e0)), b = ld_stream((const f32x4 *)(x + e0 + 4));
         float v[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
-        st_stream((u32x4 *)(codes + e0), pack_fp16x8(v));
+        st_msg((u32x4 *)(codes + e0), pack_fp16x8(v));
     } else {
         for (uint64_t e = e0; e < n; e++) codes[e] = (uint16_t)f2h(x[e]);
     }
@@ -353,7 +359,7 @@ __device__ __forceinline__ void load_grad(const GradArgs &ga, const PeerTable &p
             float acc[8];
             reduce_fp16x8(pt, 0, pt.n, e0, acc);
             const u32x4 c = pack_fp16x8(acc);
-            st_stream((u32x4 *)(ga.out_codes + e0), c);
+            st_msg((u32x4 *)(ga.out_codes + e0), c);
             if (ga.out_mean) {
                 *(f32x4 *)(ga.out_mean + e0) = f32x4{acc[0], acc[1], acc[2], acc[3]};
                 *(f32x4 *)(ga.out_mean + e0 + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
@@ -478,7 +484,7 @@ __global__ __launch_bounds__(kWG) void opt_trust_kernel(const Chunk ch, const Op
     typedef double f64x2 __attribute__((ext_vector_type(2)));
     const f64x2 *part = (const f64x2 *)ws.partials + first;
     double a0 = 0.0, a1 = 0.0;
-    constexpr int U = 8;  // loads in flight per lane
+    constexpr int U = DEDLOC_TRUST_UNROLL;  // loads in flight per lane
     for (uint32_t i0 = 0; i0 < ntiles; i0 += U * kWG) {
         f64x2 q[U];
 #pragma unroll
@@ -593,7 +599,7 @@ __global__ __launch_bounds__(kWG) void finalize_fp16_kernel(float *__restrict__ 
 #pragma unroll
     for (int j = 0; j < 8; j++) a[j] = a[j] / count;
     if (cnt == kVec) {
-        st_stream((u32x4 *)(codes + e0), pack_fp16x8(a));
+        st_msg((u32x4 *)(codes + e0), pack_fp16x8(a));
     } else {
         for (int j = 0; j < cnt; j++) codes[e0 + j] = (uint16_t)f2h(a[j]);
     }
