@@ -48,8 +48,11 @@ typedef enum {
 
 enum { DEDLOC_CODEC_F32 = 0, DEDLOC_CODEC_FP16 = 1, DEDLOC_CODEC_I8 = 2 };
 
-/* Maximum number of peers in one reduce or round call. */
+/* Maximum number of peers in one reduce or round call (and in one group of
+ * the group all-reduce). */
 #define DEDLOC_MAX_PEERS 64
+/* Maximum number of peers in one group all-reduce. */
+#define DEDLOC_MAX_GROUP_PEERS 1024
 /* The only supported int8 block length. */
 #define DEDLOC_I8_BLOCK 1024
 
@@ -246,8 +249,9 @@ int dedloc_round_lars(const void *const *peer_codes, const float *const *peer_sc
  *               (0xffffffff if it holds none);  n_out (host): m^(d-1);
  *   ws          dedloc_group_allreduce_workspace_bytes() bytes, 256-byte
  *               aligned (two sets of intermediate group messages).
- * n_peers <= DEDLOC_MAX_PEERS, group_size >= 2; errors as for
- * dedloc_reduce_shard.  One launch per iteration. */
+ * n_peers <= DEDLOC_MAX_GROUP_PEERS, 2 <= group_size <= DEDLOC_MAX_PEERS;
+ * errors as for dedloc_reduce_shard.  Each iteration takes one launch per
+ * batch of up to 64 groups holding up to 64 members with samples. */
 size_t dedloc_group_allreduce_workspace_bytes(uint32_t n_peers, uint32_t group_size, uint64_t len,
                                               int32_t codec, uint32_t block);
 int dedloc_group_allreduce(const void *const *peer_codes, const float *const *peer_scales,

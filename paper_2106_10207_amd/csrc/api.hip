@@ -363,8 +363,9 @@ struct GroupPlan {
 };
 
 int group_plan(uint32_t n, uint32_t m, uint64_t len, int32_t codec, GroupPlan &gp) {
-    if (n == 0 || n > DEDLOC_MAX_PEERS) return fail(DEDLOC_ERR_INVALID_ARG, "n_peers must be in [1, %d]", DEDLOC_MAX_PEERS);
-    if (m < 2) return fail(DEDLOC_ERR_INVALID_ARG, "group_size must be >= 2");
+    if (n == 0 || n > DEDLOC_MAX_GROUP_PEERS)
+        return fail(DEDLOC_ERR_INVALID_ARG, "n_peers must be in [1, %d]", DEDLOC_MAX_GROUP_PEERS);
+    if (m < 2 || m > DEDLOC_MAX_PEERS) return fail(DEDLOC_ERR_INVALID_ARG, "group_size must be in [2, %d]", DEDLOC_MAX_PEERS);
     uint32_t d = 1;
     uint64_t slots = m;
     while (slots < n) {
@@ -373,7 +374,7 @@ int group_plan(uint32_t n, uint32_t m, uint64_t len, int32_t codec, GroupPlan &g
     }
     gp.d = d;
     gp.slots = (uint32_t)slots;
-    gp.groups = (uint32_t)(slots / m);  // < n <= 64 when d > 1, and 1 when d == 1
+    gp.groups = (uint32_t)(slots / m);
     const size_t cb = codec == DEDLOC_CODEC_FP16 ? 2 : 1;
     gp.code_stride = round_up((size_t)len * cb, 256);
     gp.scale_stride = codec == DEDLOC_CODEC_I8 ? (size_t)((len + DEDLOC_I8_BLOCK - 1) / DEDLOC_I8_BLOCK) : 0;
@@ -589,9 +590,21 @@ int dedloc_group_allreduce(const void *const *peer_codes, const float *const *pe
     GroupPlan gp;
     rc = group_plan(n_peers, group_size, len, codec, gp);
     if (rc) return rc;
-    PeerTable all;  // validates pointers, alignment, counts (total in [1, 2^24])
-    rc = build_peers(peer_codes, peer_scales, counts, n_peers, codec, all, len > 0);
-    if (rc) return rc;
+    if (!peer_codes || !counts) return fail(DEDLOC_ERR_INVALID_ARG, "peer_codes and counts must not be NULL");
+    if (codec == DEDLOC_CODEC_I8 && !peer_scales) return fail(DEDLOC_ERR_INVALID_ARG, "int8 messages need peer_scales");
+    uint64_t total = 0;
+    for (uint32_t i = 0; i < n_peers; i++) total += counts[i];
+    if (total == 0) return fail(DEDLOC_ERR_ZERO_WEIGHT, "every peer has zero samples");
+    if (total > (1u << 24)) return fail(DEDLOC_ERR_INVALID_ARG, "total sample count exceeds 2^24");
+    if (len > 0) {
+        for (uint32_t i = 0; i < n_peers; i++) {
+            if (counts[i] == 0) continue;  // never read
+            if (!peer_codes[i] || !aligned(peer_codes[i], 16))
+                return fail(DEDLOC_ERR_ALIGN, "peer %u message must be non-NULL and 16-byte aligned", i);
+            if (codec == DEDLOC_CODEC_I8 && (!peer_scales[i] || !aligned(peer_scales[i], 4)))
+                return fail(DEDLOC_ERR_ALIGN, "peer %u scales must be non-NULL and 4-byte aligned", i);
+        }
+    }
     if (!peer_out || !n_out) return fail(DEDLOC_ERR_INVALID_ARG, "peer_out and n_out must not be NULL");
     if (len > 0) {
         if (!out_codes || !aligned(out_codes, 256)) return fail(DEDLOC_ERR_ALIGN, "out_codes must be non-NULL and 256-byte aligned");
@@ -608,26 +621,47 @@ int dedloc_group_allreduce(const void *const *peer_codes, const float *const *pe
     hipStream_t s = (hipStream_t)stream;
     char *wsc = (char *)ws;
     float *wss = (float *)(wsc + gp.ws_codes);
-    uint32_t lo = 1;  // m^k, the weight of digit k
+    GroupTable gt;
+    // launch the groups gathered in gt (one grid row each)
+    auto flush = [&]() -> int {
+        if (gt.n_groups == 0) return DEDLOC_OK;
+        gt.gbegin[gt.n_groups] = gt.pt.n;
+        if (len > 0) {
+            hipError_t e = codec == DEDLOC_CODEC_FP16
+                               ? timed(K_REDUCE_FP16, s, [&] { return launch_reduce_fp16(gt, len, nullptr, s); })
+                               : timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(gt, len, nullptr, s); });
+            if (e != hipSuccess) return hip_fail(e, "group reduce launch");
+        }
+        memset(&gt, 0, sizeof gt);
+        return DEDLOC_OK;
+    };
+    uint64_t lo = 1;  // m^k, the weight of digit k
     for (uint32_t k = 0; k < gp.d; k++, lo *= m) {
         const bool last = k + 1 == gp.d;
         char *dst_c = last ? (char *)out_codes : wsc + (size_t)(k % 2) * gp.groups * gp.code_stride;
         float *dst_s = last ? out_scales : wss + (size_t)(k % 2) * gp.groups * gp.scale_stride;
         const char *prev_c = wsc + (size_t)((k + 1) % 2) * gp.groups * gp.code_stride;
         const float *prev_s = wss + (size_t)((k + 1) % 2) * gp.groups * gp.scale_stride;
-        GroupTable gt;
         memset(&gt, 0, sizeof gt);
-        gt.n_groups = gp.groups;
         for (uint32_t g = 0; g < gp.groups; g++) {
-            const uint32_t base = (g / lo) * lo * m + (g % lo);
-            uint32_t mc[DEDLOC_MAX_PEERS];
-            uint32_t nm = 0, first = gt.pt.n;
-            uint64_t total = 0;
+            const uint64_t base = (g / lo) * lo * m + (g % lo);
+            uint32_t members = 0;
+            uint64_t gtotal = 0;
             for (uint32_t j = 0; j < m; j++) {
-                const uint32_t sl = base + j * lo;
-                total += cnt[sl];
+                gtotal += cnt[base + j * lo];
+                members += cnt[base + j * lo] > 0;
+            }
+            // a launch describes at most kMaxPeers members and kMaxGroups groups
+            if (gt.pt.n + members > (uint32_t)kMaxPeers || gt.n_groups == (uint32_t)kMaxGroups) {
+                rc = flush();
+                if (rc) return rc;
+            }
+            const uint32_t first = gt.pt.n;
+            uint32_t mc[DEDLOC_MAX_PEERS];
+            uint32_t nm = 0;
+            for (uint32_t j = 0; j < m; j++) {
+                const uint64_t sl = base + j * lo;
                 if (cnt[sl] == 0) continue;
-                if (gt.pt.n >= (uint32_t)kMaxPeers) return fail(DEDLOC_ERR_INVALID_ARG, "too many group members");
                 if (src[sl] < 0) {
                     gt.pt.codes[gt.pt.n] = peer_codes[sl];
                     gt.pt.scales[gt.pt.n] = codec == DEDLOC_CODEC_I8 ? peer_scales[sl] : nullptr;
@@ -638,28 +672,24 @@ int dedloc_group_allreduce(const void *const *peer_codes, const float *const *pe
                 mc[nm++] = (uint32_t)cnt[sl];
                 gt.pt.n++;
             }
-            gt.gbegin[g] = first;
             if (nm > 0) {
                 float w[DEDLOC_MAX_PEERS];
                 rc = compute_weights(mc, nm, w);
                 if (rc) return rc;
                 for (uint32_t j = 0; j < nm; j++) gt.pt.w[first + j] = w[j];
             }
-            gt.out[g] = dst_c + (size_t)g * gp.code_stride;
-            gt.out_scales[g] = codec == DEDLOC_CODEC_I8 ? dst_s + (size_t)g * gp.scale_stride : nullptr;
+            const uint32_t lg = gt.n_groups++;
+            gt.gbegin[lg] = first;
+            gt.out[lg] = dst_c + (size_t)g * gp.code_stride;
+            gt.out_scales[lg] = codec == DEDLOC_CODEC_I8 ? dst_s + (size_t)g * gp.scale_stride : nullptr;
             for (uint32_t j = 0; j < m; j++) {
-                const uint32_t sl = base + j * lo;
-                nsrc[sl] = total > 0 ? (int64_t)g : -2;
-                ncnt[sl] = total;
+                const uint64_t sl = base + j * lo;
+                nsrc[sl] = gtotal > 0 ? (int64_t)g : -2;
+                ncnt[sl] = gtotal;
             }
         }
-        gt.gbegin[gp.groups] = gt.pt.n;
-        if (len > 0) {
-            hipError_t e = codec == DEDLOC_CODEC_FP16
-                               ? timed(K_REDUCE_FP16, s, [&] { return launch_reduce_fp16(gt, len, nullptr, s); })
-                               : timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(gt, len, nullptr, s); });
-            if (e != hipSuccess) return hip_fail(e, "group reduce launch");
-        }
+        rc = flush();
+        if (rc) return rc;
         src.swap(nsrc);
         cnt.swap(ncnt);
     }

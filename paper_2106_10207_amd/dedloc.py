@@ -30,6 +30,7 @@ DEDLOC_CODEC_FP16 = 1
 DEDLOC_CODEC_I8 = 2
 DEDLOC_I8_BLOCK = 1024
 DEDLOC_MAX_PEERS = 64
+DEDLOC_MAX_GROUP_PEERS = 1024
 DEDLOC_TENSOR_DECAY = 1
 DEDLOC_TENSOR_ADAPT = 2
 

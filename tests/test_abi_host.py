@@ -217,4 +217,6 @@ def test_group_allreduce_validation():
     assert call(2, out=A + 16) == D.DEDLOC_ERR_ALIGN       # outputs on 256-byte boundaries
     assert call(2, wsb=0) == D.DEDLOC_ERR_WORKSPACE
     assert lib.dedloc_group_allreduce_workspace_bytes(3, 2, 64, D.DEDLOC_CODEC_FP16, 0) == 2 * 2 * 256
-    assert lib.dedloc_group_allreduce_workspace_bytes(65, 2, 64, D.DEDLOC_CODEC_FP16, 0) == 0
+    assert lib.dedloc_group_allreduce_workspace_bytes(1025, 2, 64, D.DEDLOC_CODEC_FP16, 0) == 0
+    assert lib.dedloc_group_allreduce_workspace_bytes(8, 65, 64, D.DEDLOC_CODEC_FP16, 0) == 0
+    assert lib.dedloc_group_allreduce_workspace_bytes(1024, 32, 64, D.DEDLOC_CODEC_FP16, 0) == 2 * 32 * 256

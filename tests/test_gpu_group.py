@@ -28,7 +28,8 @@ def _inputs(n, L, seed, codec):
 
 @pytest.mark.parametrize("codec", [D.DEDLOC_CODEC_FP16, D.DEDLOC_CODEC_I8])
 @pytest.mark.parametrize("n,m,L", [(8, 2, 5000), (9, 3, 2048 * 3 + 5), (64, 8, 4096), (10, 3, 1),
-                                   (64, 2, 3000), (30, 4, 1024 * 5 + 7), (5, 8, 777), (1, 2, 100)])
+                                   (64, 2, 3000), (30, 4, 1024 * 5 + 7), (5, 8, 777), (1, 2, 100),
+                                   (200, 8, 2100), (1024, 32, 300), (130, 64, 1024)])
 def test_group_allreduce(codec, n, m, L):
     codes, scales, counts = _inputs(n, L, n * 100 + m, codec)
     dc = []
