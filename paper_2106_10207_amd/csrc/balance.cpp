@@ -34,7 +34,7 @@ struct Tableau {
 // Maximise obj . x subject to A x <= b (b >= 0), x >= 0, starting from the
 // slack basis.  Dantzig's entering rule, switching to Bland's rule (smallest
 // index) after a run of degenerate pivots so that the method terminates.
-int simplex(Tableau &T, int nvar, int max_iter, double eps) {
+int simplex(Tableau &T, int max_iter, double eps) {
     const int m = T.m, rhs = T.ncol - 1;
     int degenerate = 0;
     for (int it = 0; it < max_iter; it++) {
@@ -83,7 +83,6 @@ int simplex(Tableau &T, int nvar, int max_iter, double eps) {
         }
         T.basis[p] = e;
     }
-    (void)nvar;
     return 2;  // iteration limit
 }
 
@@ -176,7 +175,7 @@ extern "C" int dedloc_balance(const dedloc_balance_problem *pr, double *xi_out, 
         T.basis[r] = nv + r;
     }
     T.at(T.m, vxi) = -1.0;  // maximise xi
-    const int rc = simplex(T, nv, 200000, 1e-12);
+    const int rc = simplex(T, 200000, 1e-12);
     if (rc != 0) return DEDLOC_ERR_INVALID_ARG;
 
     std::vector<double> x(nv, 0.0);
