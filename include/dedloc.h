@@ -48,11 +48,13 @@ typedef enum {
 
 enum { DEDLOC_CODEC_F32 = 0, DEDLOC_CODEC_FP16 = 1, DEDLOC_CODEC_I8 = 2 };
 
-/* Maximum number of peers in one reduce or round call (and in one group of
- * the group all-reduce). */
-#define DEDLOC_MAX_PEERS 64
-/* Maximum number of peers in one group all-reduce. */
+/* Maximum number of peers in one reduce or round call.  Up to 64 peers with
+ * samples are reduced in one launch; more are reduced in launches of 64
+ * chained through the fp32 average buffer (out_mean, then required). */
+#define DEDLOC_MAX_PEERS 1024
+/* Maximum number of peers in one group all-reduce, and in one of its groups. */
 #define DEDLOC_MAX_GROUP_PEERS 1024
+#define DEDLOC_MAX_GROUP_SIZE 64
 /* The only supported int8 block length. */
 #define DEDLOC_I8_BLOCK 1024
 
@@ -135,9 +137,13 @@ int dedloc_decode(const void *codes, const float *scales, uint64_t n,
  * (Appendix B: a peer that does not compute still aggregates, and its local
  * gradient is disregarded); their pointers may be NULL.
  * Outputs: out_codes / out_scales - the encoded average (as dedloc_encode);
- * out_mean (nullable) - the fp32 average before encoding.
+ * out_mean - the fp32 average before encoding; nullable with at most 64
+ * peers holding samples, required with more (it then carries the running
+ * sum between launches, stored exactly, so the result is the same as one
+ * pass).
  * Errors: n_peers == 0 or > DEDLOC_MAX_PEERS -> INVALID_ARG; all counts
- * zero -> ZERO_WEIGHT.  shard_len == 0 is a no-op (after validation). */
+ * zero -> ZERO_WEIGHT; more than 64 peers with samples and out_mean NULL ->
+ * INVALID_ARG.  shard_len == 0 is a no-op (after validation). */
 int dedloc_reduce_shard(const void *const *peer_codes, const float *const *peer_scales,
                         const uint32_t *counts, uint32_t n_peers, uint64_t shard_len,
                         int32_t codec, uint32_t block, void *out_codes,
@@ -207,7 +213,9 @@ int dedloc_lars_step(float *x, float *v, const void *grad, const float *grad_sca
  *               messages (P elements); peer_scales likewise for int8;
  *   bounds      host uint64[n_shards+1] tiling [0, P); for int8 every
  *               interior bound must be a multiple of `block`;
- *   out_mean    nullable fp32[P]: the average before encoding.
+ *   out_mean    fp32[P]: the average before encoding; nullable with at
+ *               most 64 peers holding samples, required with more (as in
+ *               dedloc_reduce_shard).
  * Workspace as dedloc_lamb_workspace_bytes. */
 int dedloc_round(const void *const *peer_codes, const float *const *peer_scales,
                  const uint32_t *counts, uint32_t n_peers, const uint64_t *bounds,
@@ -249,7 +257,7 @@ int dedloc_round_lars(const void *const *peer_codes, const float *const *peer_sc
  *               (0xffffffff if it holds none);  n_out (host): m^(d-1);
  *   ws          dedloc_group_allreduce_workspace_bytes() bytes, 256-byte
  *               aligned (two sets of intermediate group messages).
- * n_peers <= DEDLOC_MAX_GROUP_PEERS, 2 <= group_size <= DEDLOC_MAX_PEERS;
+ * n_peers <= DEDLOC_MAX_GROUP_PEERS, 2 <= group_size <= DEDLOC_MAX_GROUP_SIZE;
  * errors as for dedloc_reduce_shard.  Each iteration takes one launch per
  * batch of up to 64 groups holding up to 64 members with samples. */
 size_t dedloc_group_allreduce_workspace_bytes(uint32_t n_peers, uint32_t group_size, uint64_t len,

@@ -7,6 +7,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -107,36 +108,59 @@ int check_codec(int32_t codec, uint32_t block, bool allow_f32) {
     return fail(DEDLOC_ERR_INVALID_ARG, "unknown codec %d", codec);
 }
 
-// Active-peer table: peers with counts > 0 in ascending order.
+static_assert(DEDLOC_MAX_GROUP_SIZE <= kMaxPeers, "a group must fit one launch's peer table");
+
+// Active peers: those with counts > 0, in ascending order, with weights.
+struct PeerList {
+    std::vector<const void *> codes;
+    std::vector<const float *> scales;
+    std::vector<float> w;
+    uint32_t n() const { return (uint32_t)w.size(); }
+};
+
 int build_peers(const void *const *codes, const float *const *scales, const uint32_t *counts,
-                uint32_t n, int32_t codec, PeerTable &pt, bool check_ptrs = true) {
+                uint32_t n, int32_t codec, PeerList &pl, bool check_ptrs = true) {
     if (!codes || !counts) return fail(DEDLOC_ERR_INVALID_ARG, "peer_codes and counts must not be NULL");
     if (n == 0 || n > DEDLOC_MAX_PEERS)
         return fail(DEDLOC_ERR_INVALID_ARG, "n_peers must be in [1, %d] (got %u)", DEDLOC_MAX_PEERS, n);
     if (codec == DEDLOC_CODEC_I8 && !scales)
         return fail(DEDLOC_ERR_INVALID_ARG, "int8 messages need peer_scales");
-    float w[DEDLOC_MAX_PEERS];
-    int rc = compute_weights(counts, n, w);
+    std::vector<float> w(n);
+    int rc = compute_weights(counts, n, w.data());
     if (rc) return rc;
-    memset(&pt, 0, sizeof pt);
+    pl = PeerList();
+    if (!check_ptrs) return DEDLOC_OK;  // nothing will be read at all
     for (uint32_t p = 0; p < n; p++) {
         if (counts[p] == 0) continue;  // weight 0: never read
-        if (!check_ptrs) continue;     // nothing will be read at all
         if (!codes[p]) return fail(DEDLOC_ERR_INVALID_ARG, "peer %u has samples but a NULL message", p);
         if (!aligned(codes[p], 16)) return fail(DEDLOC_ERR_ALIGN, "peer %u message is not 16-byte aligned", p);
+        const float *sc = nullptr;
         if (codec == DEDLOC_CODEC_I8) {
             if (!scales[p]) return fail(DEDLOC_ERR_INVALID_ARG, "peer %u has samples but NULL scales", p);
             if (!aligned(scales[p], 4)) return fail(DEDLOC_ERR_ALIGN, "peer %u scales not 4-byte aligned", p);
-            pt.scales[pt.n] = scales[p];
+            sc = scales[p];
         }
-        pt.codes[pt.n] = codes[p];
-        pt.w[pt.n] = w[p];
-        pt.n++;
+        pl.codes.push_back(codes[p]);
+        pl.scales.push_back(sc);
+        pl.w.push_back(w[p]);
     }
     return DEDLOC_OK;
 }
 
-// A plain reduce: every active peer in one group writing `out`.
+// Active peers [lo, hi) as one launch's table (hi - lo <= kMaxPeers).
+PeerTable table_of(const PeerList &pl, uint32_t lo, uint32_t hi) {
+    PeerTable pt;
+    memset(&pt, 0, sizeof pt);
+    for (uint32_t p = lo; p < hi; p++) {
+        pt.codes[pt.n] = pl.codes[p];
+        pt.scales[pt.n] = pl.scales[p];
+        pt.w[pt.n] = pl.w[p];
+        pt.n++;
+    }
+    return pt;
+}
+
+// A plain reduce: every peer of the table in one group writing `out`.
 GroupTable single_group(const PeerTable &pt, void *out, float *out_scales) {
     GroupTable gt;
     memset(&gt, 0, sizeof gt);
@@ -147,6 +171,35 @@ GroupTable single_group(const PeerTable &pt, void *out, float *out_scales) {
     gt.out_scales[0] = out_scales;
     gt.n_groups = 1;
     return gt;
+}
+
+// More active peers than one launch's table holds need the fp32 mean buffer
+// to carry the running sum between launches.
+int check_chain(const PeerList &pl, const float *mean) {
+    if (pl.n() > (uint32_t)kMaxPeers && !mean)
+        return fail(DEDLOC_ERR_INVALID_ARG, "%u peers with samples (more than %d) need out_mean", pl.n(), kMaxPeers);
+    return DEDLOC_OK;
+}
+
+// Start of the last launch's peers when peers [0, n) are reduced in
+// launches of kMaxPeers.
+uint32_t last_batch(uint32_t n) { return n == 0 ? 0 : (n - 1) / kMaxPeers * kMaxPeers; }
+
+// Reduce peers [lo, hi) of the list in launches of kMaxPeers, chained through
+// `mean`; the launch holding peer hi - 1 encodes into out / out_scales when
+// `encode` is set.  Peers before lo must already be summed into `mean`.
+int run_reduce(int32_t codec, const PeerList &pl, uint32_t lo, uint32_t hi, bool encode, uint64_t len,
+               void *out, float *out_scales, float *mean, hipStream_t s) {
+    for (uint32_t a = lo; a < hi; a += kMaxPeers) {
+        const uint32_t b = std::min(hi, a + (uint32_t)kMaxPeers);
+        const GroupTable gt = single_group(table_of(pl, a, b), out, out_scales);
+        const ChainArgs ca = {a > 0 ? mean : nullptr, mean, encode && b == hi};
+        const hipError_t e = codec == DEDLOC_CODEC_FP16
+                                 ? timed(K_REDUCE_FP16, s, [&] { return launch_reduce_fp16(gt, len, ca, s); })
+                                 : timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(gt, len, ca, s); });
+        if (e != hipSuccess) return hip_fail(e, "reduce launch");
+    }
+    return DEDLOC_OK;
 }
 
 // LAMB tile table: tensors in launch chunks of at most kChunkTensors.
@@ -270,7 +323,7 @@ int run_opt(int opt, int src_a, int src_b, const Plan &pl, const PeerTable *pt, 
             const GradArgs &ga_b, const OptParams &op, float *x, float *m, float *v, void *ws,
             float *trust_out, hipStream_t s) {
     const LambWs w = carve(pl, ws);
-    const int k_a = (opt == kOptLamb ? K_LAMB_A_F32 : K_LARS_A_F32) + src_a;
+    const int k_a = (opt == kOptLamb ? K_LAMB_A_F32 : K_LARS_A_F32) + std::min(src_a, (int)kSrcPeersFP16);
     const int k_t = opt == kOptLamb ? K_LAMB_TRUST : K_LARS_TRUST;
     const int k_b = opt == kOptLamb ? K_LAMB_B : K_LARS_B;
     for (size_t c = 0; c < pl.chunks.size(); c++) {
@@ -309,10 +362,10 @@ int prepare_round(int opt, const void *const *peer_codes, const float *const *pe
                   const uint32_t *counts, uint32_t n_peers, const uint64_t *bounds, uint32_t n_shards,
                   int32_t codec, uint32_t block, void *out_codes, float *out_scales, float *x, float *m,
                   float *v, uint64_t P, const uint64_t *offsets, const uint8_t *flags, uint32_t n_tensors,
-                  float *out_mean, void *ws, size_t ws_bytes, PeerTable &pt, Plan &pl) {
+                  float *out_mean, void *ws, size_t ws_bytes, PeerList &peers, Plan &pl) {
     int rc = check_codec(codec, block, false);
     if (rc) return rc;
-    rc = build_peers(peer_codes, peer_scales, counts, n_peers, codec, pt);
+    rc = build_peers(peer_codes, peer_scales, counts, n_peers, codec, peers);
     if (rc) return rc;
     if (!bounds || n_shards == 0) return fail(DEDLOC_ERR_INVALID_ARG, "bounds must list n_shards >= 1 shards");
     if (bounds[0] != 0 || bounds[n_shards] != P) return fail(DEDLOC_ERR_INVALID_ARG, "shard bounds must tile [0, P)");
@@ -331,26 +384,31 @@ int prepare_round(int opt, const void *const *peer_codes, const float *const *pe
     if (out_mean && !aligned(out_mean, 16)) return fail(DEDLOC_ERR_ALIGN, "out_mean must be 16-byte aligned");
     if (codec == DEDLOC_CODEC_I8 && (!out_scales || !aligned(out_scales, 4)))
         return fail(DEDLOC_ERR_INVALID_ARG, "int8 round needs aligned out_scales");
-    return DEDLOC_OK;
+    return check_chain(peers, out_mean);
 }
 
 // The round after validation: the reduce-scatter and gather, then the
 // optimizer.  fp16: the codec is elementwise, so every shard's average is the
 // same function of the element index and pass A fuses the average of all
-// shards.  int8: interior shard bounds sit on block boundaries, so every
-// shard's blocks are the vector's blocks and one reduce launch covers all
-// shards before the optimizer reads the gathered message.
-int run_round(int opt, const PeerTable &pt, int32_t codec, void *out_codes, float *out_scales, float *x,
+// shards (of the last launch's peers, after the earlier ones are summed into
+// out_mean).  int8: interior shard bounds sit on block boundaries, so every
+// shard's blocks are the vector's blocks and one reduce covers all shards
+// before the optimizer reads the gathered message.
+int run_round(int opt, const PeerList &peers, int32_t codec, void *out_codes, float *out_scales, float *x,
               float *m, float *v, uint64_t P, const Plan &pl, const OptParams &op, float *trust_out,
               float *out_mean, void *ws, hipStream_t s) {
-    const GradArgs gathered = {out_codes, out_scales, nullptr, nullptr};
+    const GradArgs gathered = {out_codes, out_scales, nullptr, nullptr, nullptr};
     if (codec == DEDLOC_CODEC_FP16) {
-        const GradArgs fused = {nullptr, nullptr, (uint16_t *)out_codes, out_mean};
-        return run_opt(opt, kSrcPeersFP16, kSrcFP16, pl, &pt, fused, gathered, op, x, m, v, ws, trust_out, s);
+        const uint32_t f = last_batch(peers.n());
+        int rc = run_reduce(codec, peers, 0, f, false, P, out_codes, nullptr, out_mean, s);
+        if (rc) return rc;
+        const PeerTable pt = table_of(peers, f, peers.n());
+        const GradArgs fused = {nullptr, nullptr, (uint16_t *)out_codes, out_mean, out_mean};
+        return run_opt(opt, f > 0 ? kSrcPeersFP16Chain : kSrcPeersFP16, kSrcFP16, pl, &pt, fused, gathered, op, x,
+                       m, v, ws, trust_out, s);
     }
-    const GroupTable gt = single_group(pt, out_codes, out_scales);
-    hipError_t e = timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(gt, P, out_mean, s); });
-    if (e != hipSuccess) return hip_fail(e, "reduce launch");
+    int rc = run_reduce(codec, peers, 0, peers.n(), true, P, out_codes, out_scales, out_mean, s);
+    if (rc) return rc;
     return run_opt(opt, kSrcI8, kSrcI8, pl, nullptr, gathered, gathered, op, x, m, v, ws, trust_out, s);
 }
 
@@ -365,7 +423,7 @@ struct GroupPlan {
 int group_plan(uint32_t n, uint32_t m, uint64_t len, int32_t codec, GroupPlan &gp) {
     if (n == 0 || n > DEDLOC_MAX_GROUP_PEERS)
         return fail(DEDLOC_ERR_INVALID_ARG, "n_peers must be in [1, %d]", DEDLOC_MAX_GROUP_PEERS);
-    if (m < 2 || m > DEDLOC_MAX_PEERS) return fail(DEDLOC_ERR_INVALID_ARG, "group_size must be in [2, %d]", DEDLOC_MAX_PEERS);
+    if (m < 2 || m > DEDLOC_MAX_GROUP_SIZE) return fail(DEDLOC_ERR_INVALID_ARG, "group_size must be in [2, %d]", DEDLOC_MAX_GROUP_SIZE);
     uint32_t d = 1;
     uint64_t slots = m;
     while (slots < n) {
@@ -470,23 +528,18 @@ int dedloc_reduce_shard(const void *const *peer_codes, const float *const *peer_
                         void *stream) {
     int rc = check_codec(codec, block, false);
     if (rc) return rc;
-    PeerTable pt;
-    rc = build_peers(peer_codes, peer_scales, counts, n_peers, codec, pt, shard_len > 0);
+    PeerList peers;
+    rc = build_peers(peer_codes, peer_scales, counts, n_peers, codec, peers, shard_len > 0);
     if (rc) return rc;
     if (shard_len == 0) return DEDLOC_OK;
     if (!out_codes || !aligned(out_codes, 16)) return fail(DEDLOC_ERR_ALIGN, "out_codes must be non-NULL and 16-byte aligned");
     if (out_mean && !aligned(out_mean, 16)) return fail(DEDLOC_ERR_ALIGN, "out_mean must be 16-byte aligned");
-    hipStream_t s = (hipStream_t)stream;
-    hipError_t e;
-    if (codec == DEDLOC_CODEC_FP16) {
-        const GroupTable gt = single_group(pt, out_codes, nullptr);
-        e = timed(K_REDUCE_FP16, s, [&] { return launch_reduce_fp16(gt, shard_len, out_mean, s); });
-    } else {
-        if (!out_scales || !aligned(out_scales, 4)) return fail(DEDLOC_ERR_INVALID_ARG, "int8 reduce needs aligned out_scales");
-        const GroupTable gt = single_group(pt, out_codes, out_scales);
-        e = timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(gt, shard_len, out_mean, s); });
-    }
-    return e == hipSuccess ? DEDLOC_OK : hip_fail(e, "reduce launch");
+    if (codec == DEDLOC_CODEC_I8 && (!out_scales || !aligned(out_scales, 4)))
+        return fail(DEDLOC_ERR_INVALID_ARG, "int8 reduce needs aligned out_scales");
+    rc = check_chain(peers, out_mean);
+    if (rc) return rc;
+    return run_reduce(codec, peers, 0, peers.n(), true, shard_len, out_codes, out_scales, out_mean,
+                      (hipStream_t)stream);
 }
 
 size_t dedloc_lamb_workspace_bytes(uint64_t P, const uint64_t *offsets, uint32_t n_tensors) {
@@ -514,7 +567,7 @@ int dedloc_lamb_step(float *x, float *m, float *v, const void *grad, const float
     rc = prepare_step(kOptLamb, x, m, v, grad, grad_scales, grad_codec, block, P, offsets, flags, n_tensors,
                       ws, ws_bytes, pl);
     if (rc) return rc;
-    const GradArgs ga = {grad, grad_scales, nullptr, nullptr};
+    const GradArgs ga = {grad, grad_scales, nullptr, nullptr, nullptr};
     const int src = grad_src(grad_codec);
     return run_opt(kOptLamb, src, src, pl, nullptr, ga, ga, op, x, m, v, ws, trust_out, (hipStream_t)stream);
 }
@@ -530,7 +583,7 @@ int dedloc_lars_step(float *x, float *v, const void *grad, const float *grad_sca
     rc = prepare_step(kOptLars, x, nullptr, v, grad, grad_scales, grad_codec, block, P, offsets, flags,
                       n_tensors, ws, ws_bytes, pl);
     if (rc) return rc;
-    const GradArgs ga = {grad, grad_scales, nullptr, nullptr};
+    const GradArgs ga = {grad, grad_scales, nullptr, nullptr, nullptr};
     const int src = grad_src(grad_codec);
     return run_opt(kOptLars, src, src, pl, nullptr, ga, ga, op, x, nullptr, v, ws, trust_out, (hipStream_t)stream);
 }
@@ -544,13 +597,13 @@ int dedloc_round(const void *const *peer_codes, const float *const *peer_scales,
     OptParams op;
     int rc = lamb_params(cfg, op);
     if (rc) return rc;
-    PeerTable pt;
+    PeerList peers;
     Plan pl;
     rc = prepare_round(kOptLamb, peer_codes, peer_scales, counts, n_peers, bounds, n_shards, codec, block,
                        out_codes, out_scales, x, m, v, P, offsets, flags, n_tensors, out_mean, ws, ws_bytes,
-                       pt, pl);
+                       peers, pl);
     if (rc) return rc;
-    return run_round(kOptLamb, pt, codec, out_codes, out_scales, x, m, v, P, pl, op, trust_out, out_mean, ws,
+    return run_round(kOptLamb, peers, codec, out_codes, out_scales, x, m, v, P, pl, op, trust_out, out_mean, ws,
                      (hipStream_t)stream);
 }
 
@@ -563,13 +616,13 @@ int dedloc_round_lars(const void *const *peer_codes, const float *const *peer_sc
     OptParams op;
     int rc = lars_params(cfg, op);
     if (rc) return rc;
-    PeerTable pt;
+    PeerList peers;
     Plan pl;
     rc = prepare_round(kOptLars, peer_codes, peer_scales, counts, n_peers, bounds, n_shards, codec, block,
                        out_codes, out_scales, x, nullptr, v, P, offsets, flags, n_tensors, out_mean, ws,
-                       ws_bytes, pt, pl);
+                       ws_bytes, peers, pl);
     if (rc) return rc;
-    return run_round(kOptLars, pt, codec, out_codes, out_scales, x, nullptr, v, P, pl, op, trust_out, out_mean,
+    return run_round(kOptLars, peers, codec, out_codes, out_scales, x, nullptr, v, P, pl, op, trust_out, out_mean,
                      ws, (hipStream_t)stream);
 }
 
@@ -627,9 +680,10 @@ int dedloc_group_allreduce(const void *const *peer_codes, const float *const *pe
         if (gt.n_groups == 0) return DEDLOC_OK;
         gt.gbegin[gt.n_groups] = gt.pt.n;
         if (len > 0) {
+            const ChainArgs ca = {nullptr, nullptr, 1};
             hipError_t e = codec == DEDLOC_CODEC_FP16
-                               ? timed(K_REDUCE_FP16, s, [&] { return launch_reduce_fp16(gt, len, nullptr, s); })
-                               : timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(gt, len, nullptr, s); });
+                               ? timed(K_REDUCE_FP16, s, [&] { return launch_reduce_fp16(gt, len, ca, s); })
+                               : timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(gt, len, ca, s); });
             if (e != hipSuccess) return hip_fail(e, "group reduce launch");
         }
         memset(&gt, 0, sizeof gt);
@@ -657,7 +711,7 @@ int dedloc_group_allreduce(const void *const *peer_codes, const float *const *pe
                 if (rc) return rc;
             }
             const uint32_t first = gt.pt.n;
-            uint32_t mc[DEDLOC_MAX_PEERS];
+            uint32_t mc[DEDLOC_MAX_GROUP_SIZE];
             uint32_t nm = 0;
             for (uint32_t j = 0; j < m; j++) {
                 const uint64_t sl = base + j * lo;
@@ -673,7 +727,7 @@ int dedloc_group_allreduce(const void *const *peer_codes, const float *const *pe
                 gt.pt.n++;
             }
             if (nm > 0) {
-                float w[DEDLOC_MAX_PEERS];
+                float w[DEDLOC_MAX_GROUP_SIZE];
                 rc = compute_weights(mc, nm, w);
                 if (rc) return rc;
                 for (uint32_t j = 0; j < nm; j++) gt.pt.w[first + j] = w[j];

@@ -63,6 +63,15 @@ struct GroupTable {
     uint32_t n_groups;
 };
 
+// A reduce over more peers than one table holds is a chain of launches
+// through an fp32 running sum (stored exactly between launches, so the fma
+// chain is the same as in one pass).  Only a single-group reduce chains.
+struct ChainArgs {
+    const float *acc_in;  // running sum of the peers before this launch (nullable: start at +0)
+    float *acc_out;       // the sum after this launch (the mean after the last launch; nullable)
+    int final_pass;       // encode into the group outputs
+};
+
 // A run of consecutive tensors handled by one LAMB launch (it spans fewer
 // than 2^32 elements).  Tiles never cross a tensor: tensor k of the chunk
 // covers elements base + [start[k], start[k+1]) and owns launch blocks
@@ -96,14 +105,16 @@ enum GradSrc : int {
     kSrcF32 = 0,      // fp32 gradient
     kSrcFP16 = 1,     // fp16 message
     kSrcI8 = 2,       // int8 message + block scales
-    kSrcPeersFP16 = 3 // fused: average the fp16 peer messages, encode, decode
+    kSrcPeersFP16 = 3,     // fused: average the fp16 peer messages, encode, decode
+    kSrcPeersFP16Chain = 4 // the same, continuing a running sum of earlier peers
 };
 
 struct GradArgs {
     const void *grad;        // kSrcF32 / kSrcFP16 / kSrcI8
     const float *scales;     // kSrcI8
-    uint16_t *out_codes;     // kSrcPeersFP16: gathered encoded average
-    float *out_mean;         // kSrcPeersFP16: fp32 average (nullable)
+    uint16_t *out_codes;     // kSrcPeersFP16*: gathered encoded average
+    float *out_mean;         // kSrcPeersFP16*: fp32 average (nullable)
+    const float *acc_in;     // kSrcPeersFP16Chain: running sum of the earlier peers
 };
 
 struct LambWs {
@@ -117,8 +128,8 @@ hipError_t launch_decode_fp16(const uint16_t *codes, uint64_t n, float *out, hip
 hipError_t launch_encode_i8(const float *x, uint64_t n, int8_t *codes, float *scales, hipStream_t s);
 hipError_t launch_decode_i8(const int8_t *codes, const float *scales, uint64_t n, float *out,
                             hipStream_t s);
-hipError_t launch_reduce_fp16(const GroupTable &gt, uint64_t len, float *mean, hipStream_t s);
-hipError_t launch_reduce_i8(const GroupTable &gt, uint64_t len, float *mean, hipStream_t s);
+hipError_t launch_reduce_fp16(const GroupTable &gt, uint64_t len, const ChainArgs &ca, hipStream_t s);
+hipError_t launch_reduce_i8(const GroupTable &gt, uint64_t len, const ChainArgs &ca, hipStream_t s);
 hipError_t launch_opt_a(int opt, int src, const Chunk &ch, uint32_t n_tiles, const PeerTable *pt,
                         const GradArgs &ga, const OptParams &op, float *x, float *m, float *v,
                         const LambWs &ws, hipStream_t s);

@@ -193,12 +193,22 @@ __global__ __launch_bounds__(kWG) void decode_i8_kernel(const int8_t *__restrict
 // w_p * dec_p[e], one fma per peer starting from +0.  A launch reduces every
 // group of a GroupTable: grid row blockIdx.y is the group.
 
+// Running sums of eight consecutive elements: from acc_in, or +0.
+__device__ __forceinline__ void init8(const float *acc_in, uint64_t e0, float *acc) {
+    if (acc_in) {
+        const f32x4 a = *(const f32x4 *)(acc_in + e0), b = *(const f32x4 *)(acc_in + e0 + 4);
+        acc[0] = a[0]; acc[1] = a[1]; acc[2] = a[2]; acc[3] = a[3];
+        acc[4] = b[0]; acc[5] = b[1]; acc[6] = b[2]; acc[7] = b[3];
+    } else {
+#pragma unroll
+        for (int i = 0; i < 8; i++) acc[i] = 0.0f;
+    }
+}
+
 // Eight consecutive fp16 elements starting at e0 (all in range), peers
-// [p_lo, p_hi) of the table.
+// [p_lo, p_hi) of the table, added to the running sums in acc.
 __device__ __forceinline__ void reduce_fp16x8(const PeerTable &pt, uint32_t p_lo, uint32_t p_hi,
                                               uint64_t e0, float *acc) {
-#pragma unroll
-    for (int i = 0; i < 8; i++) acc[i] = 0.0f;
     constexpr int B = kPeerBatch;  // peer loads kept in flight per lane
     for (uint32_t p0 = p_lo; p0 < p_hi; p0 += B) {
         u32x4 c[B];
@@ -219,32 +229,33 @@ __device__ __forceinline__ void reduce_fp16x8(const PeerTable &pt, uint32_t p_lo
 }
 
 __device__ __forceinline__ float reduce_fp16_one(const PeerTable &pt, uint32_t p_lo, uint32_t p_hi,
-                                                 uint64_t e) {
-    float acc = 0.0f;
+                                                 uint64_t e, float acc) {
     for (uint32_t p = p_lo; p < p_hi; p++)
         acc = fmaf(pt.w[p], h2f(((const uint16_t *)pt.codes[p])[e]), acc);
     return acc;
 }
 
 __global__ __launch_bounds__(kWG) void reduce_fp16_kernel(const GroupTable gt, uint64_t len,
-                                                          float *__restrict__ mean) {
+                                                          const ChainArgs ca) {
     const uint32_t g = blockIdx.y;
     const uint32_t p_lo = gt.gbegin[g], p_hi = gt.gbegin[g + 1];
     if (p_lo == p_hi) return;  // a group without samples produces nothing
     uint16_t *__restrict__ out = (uint16_t *)gt.out[g];
+    float *mean = ca.acc_out;  // may alias ca.acc_in (same element, same lane)
     const uint64_t e0 = ((uint64_t)blockIdx.x * kWG + threadIdx.x) * kVec;
     if (e0 + kVec <= len) {
         float acc[8];
+        init8(ca.acc_in, e0, acc);
         reduce_fp16x8(gt.pt, p_lo, p_hi, e0, acc);
-        *(u32x4 *)(out + e0) = pack_fp16x8(acc);
+        if (ca.final_pass) *(u32x4 *)(out + e0) = pack_fp16x8(acc);
         if (mean) {
             *(f32x4 *)(mean + e0) = f32x4{acc[0], acc[1], acc[2], acc[3]};
             *(f32x4 *)(mean + e0 + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
         }
     } else {
         for (uint64_t e = e0; e < len; e++) {
-            const float a = reduce_fp16_one(gt.pt, p_lo, p_hi, e);
-            out[e] = (uint16_t)f2h(a);
+            const float a = reduce_fp16_one(gt.pt, p_lo, p_hi, e, ca.acc_in ? ca.acc_in[e] : 0.0f);
+            if (ca.final_pass) out[e] = (uint16_t)f2h(a);
             if (mean) mean[e] = a;
         }
     }
@@ -252,7 +263,7 @@ __global__ __launch_bounds__(kWG) void reduce_fp16_kernel(const GroupTable gt, u
 
 // One wave per 1024-element block; lane holds 16 elements.
 __global__ __launch_bounds__(kWG) void reduce_i8_kernel(const GroupTable gt, uint64_t len,
-                                                        float *__restrict__ mean) {
+                                                        const ChainArgs ca) {
     const uint32_t g = blockIdx.y;
     const uint32_t p_lo = gt.gbegin[g], p_hi = gt.gbegin[g + 1];
     if (p_lo == p_hi) return;  // a group without samples produces nothing
@@ -264,9 +275,10 @@ __global__ __launch_bounds__(kWG) void reduce_i8_kernel(const GroupTable gt, uin
     if (blk * kI8Block >= len) return;  // whole wave past the end
     const uint64_t e0 = blk * kI8Block + (threadIdx.x & 63) * kI8PerLane;
     const bool full = e0 + kI8PerLane <= len;
+    float *mean = ca.acc_out;  // may alias ca.acc_in (same element, same lane)
     float acc[kI8PerLane];
 #pragma unroll
-    for (int j = 0; j < kI8PerLane; j++) acc[j] = 0.0f;
+    for (int j = 0; j < kI8PerLane; j++) acc[j] = (ca.acc_in && e0 + j < len) ? ca.acc_in[e0 + j] : 0.0f;
     constexpr int B = 4;
     for (uint32_t p0 = p_lo; p0 < p_hi; p0 += B) {
         u32x4 c[B];
@@ -297,22 +309,24 @@ __global__ __launch_bounds__(kWG) void reduce_i8_kernel(const GroupTable gt, uin
             }
         }
     }
+    if (mean) {
+        if (full) {
+#pragma unroll
+            for (int q = 0; q < 4; q++)
+                *(f32x4 *)(mean + e0 + 4 * q) = f32x4{acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
+        } else {
+            for (int k = 0; k < kI8PerLane; k++)
+                if (e0 + k < len) mean[e0 + k] = acc[k];
+        }
+    }
+    if (!ca.final_pass) return;  // wave-uniform
     float s;
     const u32x4 c = encode_i8_wave(acc, s);  // out-of-range lanes hold 0
     if (full) {
         *(u32x4 *)(out + e0) = c;
-        if (mean) {
-#pragma unroll
-            for (int q = 0; q < 4; q++)
-                *(f32x4 *)(mean + e0 + 4 * q) = f32x4{acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
-        }
     } else {
-        for (int k = 0; k < kI8PerLane; k++) {
-            if (e0 + k < len) {
-                out[e0 + k] = (int8_t)(c[k >> 2] >> (8 * (k & 3)));
-                if (mean) mean[e0 + k] = acc[k];
-            }
-        }
+        for (int k = 0; k < kI8PerLane; k++)
+            if (e0 + k < len) out[e0 + k] = (int8_t)(c[k >> 2] >> (8 * (k & 3)));
     }
     if ((threadIdx.x & 63) == 0) out_scales[blk] = s;
 }
@@ -357,6 +371,7 @@ __device__ __forceinline__ void load_grad(const GradArgs &ga, const PeerTable &p
             for (int j = 0; j < 8; j++) g[j] = sbyte(c[j >> 2], j & 3) * s;
         } else {
             float acc[8];
+            init8(SRC == kSrcPeersFP16Chain ? ga.acc_in : nullptr, e0, acc);
             reduce_fp16x8(pt, 0, pt.n, e0, acc);
             const u32x4 c = pack_fp16x8(acc);
             st_msg((u32x4 *)(ga.out_codes + e0), c);
@@ -380,7 +395,7 @@ __device__ __forceinline__ void load_grad(const GradArgs &ga, const PeerTable &p
             } else if (SRC == kSrcI8) {
                 g[j] = (float)((const int8_t *)ga.grad)[e] * ga.scales[e / kI8Block];
             } else {
-                const float a = reduce_fp16_one(pt, 0, pt.n, e);
+                const float a = reduce_fp16_one(pt, 0, pt.n, e, SRC == kSrcPeersFP16Chain ? ga.acc_in[e] : 0.0f);
                 const unsigned c = f2h(a);
                 ga.out_codes[e] = (uint16_t)c;
                 if (ga.out_mean) ga.out_mean[e] = a;
@@ -669,13 +684,13 @@ hipError_t launch_decode_i8(const int8_t *codes, const float *scales, uint64_t n
     DEDLOC_LAUNCH(dim3(grid_for(n, (uint64_t)kWG * kI8PerLane)), decode_i8_kernel, s, codes, scales, n, out);
 }
 
-hipError_t launch_reduce_fp16(const GroupTable &gt, uint64_t len, float *mean, hipStream_t s) {
-    DEDLOC_LAUNCH(dim3(grid_for(len, (uint64_t)kWG * kVec), gt.n_groups), reduce_fp16_kernel, s, gt, len, mean);
+hipError_t launch_reduce_fp16(const GroupTable &gt, uint64_t len, const ChainArgs &ca, hipStream_t s) {
+    DEDLOC_LAUNCH(dim3(grid_for(len, (uint64_t)kWG * kVec), gt.n_groups), reduce_fp16_kernel, s, gt, len, ca);
 }
 
-hipError_t launch_reduce_i8(const GroupTable &gt, uint64_t len, float *mean, hipStream_t s) {
+hipError_t launch_reduce_i8(const GroupTable &gt, uint64_t len, const ChainArgs &ca, hipStream_t s) {
     DEDLOC_LAUNCH(dim3(grid_for(len, (uint64_t)kI8Block * (kWG / 64)), gt.n_groups), reduce_i8_kernel, s, gt, len,
-                  mean);
+                  ca);
 }
 
 template <int OPT>
@@ -686,6 +701,8 @@ static hipError_t launch_a(int src, const Chunk &ch, uint32_t n_tiles, const Pee
     case kSrcFP16: DEDLOC_LAUNCH(dim3(n_tiles), (opt_a_kernel<kSrcFP16, OPT>), s, ch, p, ga, op, x, m, v, ws);
     case kSrcI8: DEDLOC_LAUNCH(dim3(n_tiles), (opt_a_kernel<kSrcI8, OPT>), s, ch, p, ga, op, x, m, v, ws);
     case kSrcPeersFP16: DEDLOC_LAUNCH(dim3(n_tiles), (opt_a_kernel<kSrcPeersFP16, OPT>), s, ch, p, ga, op, x, m, v, ws);
+    case kSrcPeersFP16Chain:
+        DEDLOC_LAUNCH(dim3(n_tiles), (opt_a_kernel<kSrcPeersFP16Chain, OPT>), s, ch, p, ga, op, x, m, v, ws);
     default: return hipErrorInvalidValue;
     }
 }

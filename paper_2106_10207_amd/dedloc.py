@@ -29,8 +29,10 @@ DEDLOC_CODEC_F32 = 0
 DEDLOC_CODEC_FP16 = 1
 DEDLOC_CODEC_I8 = 2
 DEDLOC_I8_BLOCK = 1024
-DEDLOC_MAX_PEERS = 64
+DEDLOC_MAX_PEERS = 1024
 DEDLOC_MAX_GROUP_PEERS = 1024
+DEDLOC_MAX_GROUP_SIZE = 64
+DEDLOC_LAUNCH_PEERS = 64  # peers with samples reduced per launch
 DEDLOC_TENSOR_DECAY = 1
 DEDLOC_TENSOR_ADAPT = 2
 

@@ -111,7 +111,11 @@ def test_reduce_validation_before_launch():
     assert _call_reduce([A, A], None, [0, 0], 2, 64, F, 0, A, None, None) == D.DEDLOC_ERR_ZERO_WEIGHT
     assert _call_reduce([A + 2, A], None, [1, 1], 2, 64, F, 0, A, None, None) == D.DEDLOC_ERR_ALIGN
     assert _call_reduce([A, A], None, [1, 1], 2, 64, F, 0, A + 8, None, None) == D.DEDLOC_ERR_ALIGN
+    # too many peers; more than one launch's worth of peers with samples and
+    # no fp32 buffer to carry the running sum
+    assert _call_reduce([A] * 1025, None, [1] * 1025, 1025, 64, F, 0, A, None, A) == D.DEDLOC_ERR_INVALID_ARG
     assert _call_reduce([A] * 65, None, [1] * 65, 65, 64, F, 0, A, None, None) == D.DEDLOC_ERR_INVALID_ARG
+    assert "out_mean" in D.load().dedloc_last_error().decode()
     assert _call_reduce([A, None], None, [1, 1], 2, 64, F, 0, A, None, None) == D.DEDLOC_ERR_INVALID_ARG
     assert _call_reduce([A, A], None, [1, 1], 2, 64, 7, 0, A, None, None) == D.DEDLOC_ERR_INVALID_ARG
     # int8 needs scales and block 1024
@@ -167,6 +171,14 @@ def test_round_validation_before_launch():
     assert call([0, 3000, 1000, P]) == D.DEDLOC_ERR_INVALID_ARG       # decreasing
     ps = (ctypes.c_void_p * 2)(A, A)
     assert call([0, 1000, P], D.DEDLOC_CODEC_I8, 1024, ps, A) == D.DEDLOC_ERR_INVALID_ARG  # not on a block
+    # 65 peers with samples need out_mean
+    pc65 = (ctypes.c_void_p * 65)(*([A] * 65))
+    c65 = np.ones(65, np.uint32)
+    b = np.array([0, P], np.uint64)
+    assert lib.dedloc_round(pc65, None, c65.ctypes.data, 65, b.ctypes.data, 1, D.DEDLOC_CODEC_FP16, 0,
+                            A, None, A, A, A, P, off.ctypes.data, fl.ctypes.data, 2,
+                            ctypes.byref(cfg), None, None, A, need, None) == D.DEDLOC_ERR_INVALID_ARG
+    assert "out_mean" in lib.dedloc_last_error().decode()
 
 
 def _ws_expected(sizes, tile=2048):
