@@ -5,7 +5,10 @@ A step is one pass of the whole path over one batch of synthetic input:
 shard bounds on the host, the local peer's encode of its own fp32 gradient
 (the sender side), and the round: every shard averaged from the N peer
 messages, the average re-encoded and gathered, and one LAMB step with
-per-tensor trust ratios over the whole parameter vector.
+per-tensor trust ratios over the whole parameter vector.  The local
+peer's gradient is handed to the round (dedloc_local_peer): the fp16 round
+encodes it inside its averaging pass, the int8 round in a launch of its own;
+with --separate-encode the caller encodes it before the round.
 
 Default workload: ALBERT-large-shaped (17.7M parameters in 25 tensors,
 16 peers, fp16 wire).  Prints ONE JSON line.
@@ -41,6 +44,8 @@ def _parse():
                     help="capture one step (encode + round) in a HIP graph and time its replays")
     ap.add_argument("--optimizer", default="lamb", choices=["lamb", "lars"],
                     help="optimizer after the gather: LAMB (ALBERT runs) or LARS (SwAV runs)")
+    ap.add_argument("--separate-encode", action="store_true",
+                    help="encode the local peer's gradient in its own launch before the round")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-reps", type=int, default=2)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -138,6 +143,10 @@ def kernel_roofline(dr, prof, steps):
     N = active peers, P elements):
       lamb_a_fused_fp16: N*b*P peer reads + b*P code writes + 12P reads of
                          x, m, v + 8P writes of m', v'
+      (with the local peer's encode inside the averaging pass, the
+      lamb_a_fused_fp16 and lars_a_fused_fp16 launches read its 4P fp32
+      gradient and write its b*P message instead of reading that message:
+      +4P)
       reduce_i8:         N*b*P peer reads + b*P code/scale writes
       lamb_a_i8:         b*P code reads + 20P (x, m, v reads; m', v' writes)
       lamb_b:            12P reads (x, m', v') + 4P writes
@@ -149,13 +158,14 @@ def kernel_roofline(dr, prof, steps):
     P = wl.P
     b = wl.wire_bytes_per_elem
     n_act = int(np.count_nonzero(dr.counts))
+    loc = 4.0 if dr.local_in_kernel else 0.0
     per_launch = {
-        "lamb_a_fused_fp16": (n_act * b + b + 20.0) * P,
+        "lamb_a_fused_fp16": (n_act * b + b + 20.0 + loc) * P,
         "reduce_i8": (n_act * b + b) * P,
         "lamb_a_i8": (b + 20.0) * P,
         "lamb_a_fp16": (b + 20.0) * P,
         "lamb_b": 16.0 * P,
-        "lars_a_fused_fp16": (n_act * b + b + 4.0) * P,
+        "lars_a_fused_fp16": (n_act * b + b + 4.0 + loc) * P,
         "lars_a_i8": (b + 4.0) * P,
         "lars_a_fp16": (b + 4.0) * P,
         "lars_b": (b + 16.0) * P,
@@ -376,12 +386,14 @@ def main():
     if args.mode == "group":
         print(json.dumps(bench_group(args, wl)), flush=True)
         return
-    dr = H.DeviceRound(wl, "cuda", keep_local_grad=True, optimizer=args.optimizer)
+    dr = H.DeviceRound(wl, "cuda", keep_local_grad=True, optimizer=args.optimizer,
+                       fused_local=not args.separate_encode)
     bw = W.bandwidth_weights(wl)
 
     def eager_step():
         D.dedloc_partition(wl.P, wl.n_shards, bw, wl.shard_align)
-        dr.encode_local()
+        if args.separate_encode:
+            dr.encode_local()
         dr.run()
 
     step = eager_step
@@ -392,7 +404,8 @@ def main():
         eager_step()
         torch.cuda.synchronize()
         with torch.cuda.graph(graph, stream=side):
-            dr.encode_local()
+            if args.separate_encode:
+                dr.encode_local()
             dr.call(stream=side)
 
         def step():
@@ -443,7 +456,7 @@ def main():
 
     t = ms_per_step * 1e-3
     peer_bytes = dr.bytes_peer_input()
-    alg_bytes = dr.bytes_round() + dr.bytes_encode_local()
+    alg_bytes = dr.bytes_step()
     out = {
         "metric": "reduce+LAMB round GB/s of peer input (fraction of HBM peak); params/s",
         "value": round(peer_bytes / t / 1e9, 2),
@@ -467,6 +480,7 @@ def main():
             "shards": wl.n_shards,
             "optimizer": args.optimizer,
             "graph": bool(args.graph),
+            "local_encode": "separate" if args.separate_encode else "fused",
             "parallelism": "single GPU; peers are HBM regions",
         },
         "params_per_s": round(wl.P / t, 1),

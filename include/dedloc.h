@@ -202,6 +202,23 @@ int dedloc_lars_step(float *x, float *v, const void *grad, const float *grad_sca
                      const uint8_t *flags, uint32_t n_tensors, const dedloc_lars_cfg *cfg,
                      float *trust_out, void *ws, size_t ws_bytes, void *stream);
 
+/* The local peer of a round (optional argument of dedloc_round and
+ * dedloc_round_lars).  Every peer encodes its own gradient before sending
+ * it (Section 3.1: peers exchange their accumulated gradients).  Instead of a
+ * message encoded beforehand, peer `index` hands the round its fp32 mean
+ * gradient; the round encodes it into that peer's message buffers
+ * (peer_codes[index] and, for int8, peer_scales[index], which are outputs
+ * here): the fp16 round inside the pass that averages it (the message is
+ * written but never read back), the int8 round in a launch of its own before
+ * the reduce.  Every output, that message included, is bit-identical to
+ * dedloc_encode followed by the round.
+ *   index  in [0, n_peers), with counts[index] > 0;
+ *   grad   device fp32[P], 16-byte aligned, not overlapping any output. */
+typedef struct {
+    uint32_t index;
+    const float *grad;
+} dedloc_local_peer;
+
 /* One whole averaging round as seen by one GPU holding every reducer
  * (Sections 3.1-3.2): each shard [bounds[k], bounds[k+1]) of the vector is
  * averaged from the n_peers messages (as dedloc_reduce_shard), the encoded
@@ -215,7 +232,8 @@ int dedloc_lars_step(float *x, float *v, const void *grad, const float *grad_sca
  *               interior bound must be a multiple of `block`;
  *   out_mean    fp32[P]: the average before encoding; nullable with at
  *               most 64 peers holding samples, required with more (as in
- *               dedloc_reduce_shard).
+ *               dedloc_reduce_shard);
+ *   local       host, nullable: the local peer (dedloc_local_peer).
  * Workspace as dedloc_lamb_workspace_bytes. */
 int dedloc_round(const void *const *peer_codes, const float *const *peer_scales,
                  const uint32_t *counts, uint32_t n_peers, const uint64_t *bounds,
@@ -223,7 +241,7 @@ int dedloc_round(const void *const *peer_codes, const float *const *peer_scales,
                  float *out_scales, float *x, float *m, float *v, uint64_t P,
                  const uint64_t *offsets, const uint8_t *flags, uint32_t n_tensors,
                  const dedloc_lamb_cfg *cfg, float *trust_out, float *out_mean,
-                 void *ws, size_t ws_bytes, void *stream);
+                 const dedloc_local_peer *local, void *ws, size_t ws_bytes, void *stream);
 
 /* The same round with the LARS step (dedloc_lars_step) in place of LAMB;
  * v is the momentum buffer.  The fp16 path reads each peer byte once; pass B
@@ -234,7 +252,7 @@ int dedloc_round_lars(const void *const *peer_codes, const float *const *peer_sc
                       float *out_scales, float *x, float *v, uint64_t P,
                       const uint64_t *offsets, const uint8_t *flags, uint32_t n_tensors,
                       const dedloc_lars_cfg *cfg, float *trust_out, float *out_mean,
-                      void *ws, size_t ws_bytes, void *stream);
+                      const dedloc_local_peer *local, void *ws, size_t ws_bytes, void *stream);
 
 /* Group (Moshpit) all-reduce (Section 3.2 "Node failures"; Appendix C):
  * instead of one global average, peers average in groups of m = group_size

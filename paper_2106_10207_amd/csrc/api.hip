@@ -115,6 +115,7 @@ struct PeerList {
     std::vector<const void *> codes;
     std::vector<const float *> scales;
     std::vector<float> w;
+    std::vector<uint32_t> index;  // the caller's peer index
     uint32_t n() const { return (uint32_t)w.size(); }
 };
 
@@ -143,6 +144,7 @@ int build_peers(const void *const *codes, const float *const *scales, const uint
         pl.codes.push_back(codes[p]);
         pl.scales.push_back(sc);
         pl.w.push_back(w[p]);
+        pl.index.push_back(p);
     }
     return DEDLOC_OK;
 }
@@ -185,15 +187,24 @@ int check_chain(const PeerList &pl, const float *mean) {
 // launches of kMaxPeers.
 uint32_t last_batch(uint32_t n) { return n == 0 ? 0 : (n - 1) / kMaxPeers * kMaxPeers; }
 
+// The local peer as seen by a launch of active peers [a, b): its position
+// relative to a, or -1 if the launch does not hold it.
+LocalArgs local_in(const LocalArgs &la, uint32_t a, uint32_t b) {
+    LocalArgs r = la;
+    r.pos = (la.pos >= 0 && (uint32_t)la.pos >= a && (uint32_t)la.pos < b) ? la.pos - (int32_t)a : -1;
+    return r;
+}
+
 // Reduce peers [lo, hi) of the list in launches of kMaxPeers, chained through
 // `mean`; the launch holding peer hi - 1 encodes into out / out_scales when
 // `encode` is set.  Peers before lo must already be summed into `mean`.
+// la.pos: the local peer's position in the list (-1: none; fp16 only).
 int run_reduce(int32_t codec, const PeerList &pl, uint32_t lo, uint32_t hi, bool encode, uint64_t len,
-               void *out, float *out_scales, float *mean, hipStream_t s) {
+               void *out, float *out_scales, float *mean, const LocalArgs &la, hipStream_t s) {
     for (uint32_t a = lo; a < hi; a += kMaxPeers) {
         const uint32_t b = std::min(hi, a + (uint32_t)kMaxPeers);
         const GroupTable gt = single_group(table_of(pl, a, b), out, out_scales);
-        const ChainArgs ca = {a > 0 ? mean : nullptr, mean, encode && b == hi};
+        const ChainArgs ca = {a > 0 ? mean : nullptr, mean, encode && b == hi, local_in(la, a, b)};
         const hipError_t e = codec == DEDLOC_CODEC_FP16
                                  ? timed(K_REDUCE_FP16, s, [&] { return launch_reduce_fp16(gt, len, ca, s); })
                                  : timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(gt, len, ca, s); });
@@ -362,11 +373,24 @@ int prepare_round(int opt, const void *const *peer_codes, const float *const *pe
                   const uint32_t *counts, uint32_t n_peers, const uint64_t *bounds, uint32_t n_shards,
                   int32_t codec, uint32_t block, void *out_codes, float *out_scales, float *x, float *m,
                   float *v, uint64_t P, const uint64_t *offsets, const uint8_t *flags, uint32_t n_tensors,
-                  float *out_mean, void *ws, size_t ws_bytes, PeerList &peers, Plan &pl) {
+                  float *out_mean, const dedloc_local_peer *local, void *ws, size_t ws_bytes,
+                  PeerList &peers, Plan &pl, LocalArgs &la) {
     int rc = check_codec(codec, block, false);
     if (rc) return rc;
     rc = build_peers(peer_codes, peer_scales, counts, n_peers, codec, peers);
     if (rc) return rc;
+    la = LocalArgs{-1, nullptr, nullptr, nullptr};
+    if (local) {
+        if (local->index >= n_peers || counts[local->index] == 0)
+            return fail(DEDLOC_ERR_INVALID_ARG, "the local peer must be one of the peers and hold samples");
+        if (!local->grad || !aligned(local->grad, 16))
+            return fail(DEDLOC_ERR_ALIGN, "the local gradient must be non-NULL and 16-byte aligned");
+        for (uint32_t k = 0; k < peers.n(); k++)
+            if (peers.index[k] == local->index) la.pos = (int32_t)k;
+        la.grad = local->grad;
+        la.codes = const_cast<void *>(peer_codes[local->index]);
+        la.scales = codec == DEDLOC_CODEC_I8 ? const_cast<float *>(peer_scales[local->index]) : nullptr;
+    }
     if (!bounds || n_shards == 0) return fail(DEDLOC_ERR_INVALID_ARG, "bounds must list n_shards >= 1 shards");
     if (bounds[0] != 0 || bounds[n_shards] != P) return fail(DEDLOC_ERR_INVALID_ARG, "shard bounds must tile [0, P)");
     for (uint32_t k = 0; k < n_shards; k++) {
@@ -396,18 +420,28 @@ int prepare_round(int opt, const void *const *peer_codes, const float *const *pe
 // before the optimizer reads the gathered message.
 int run_round(int opt, const PeerList &peers, int32_t codec, void *out_codes, float *out_scales, float *x,
               float *m, float *v, uint64_t P, const Plan &pl, const OptParams &op, float *trust_out,
-              float *out_mean, void *ws, hipStream_t s) {
-    const GradArgs gathered = {out_codes, out_scales, nullptr, nullptr, nullptr};
+              float *out_mean, const LocalArgs &la, void *ws, hipStream_t s) {
+    const LocalArgs none = {-1, nullptr, nullptr, nullptr};
+    const GradArgs gathered = {out_codes, out_scales, nullptr, nullptr, nullptr, none};
     if (codec == DEDLOC_CODEC_FP16) {
-        const uint32_t f = last_batch(peers.n());
-        int rc = run_reduce(codec, peers, 0, f, false, P, out_codes, nullptr, out_mean, s);
+        const uint32_t n = peers.n(), f = last_batch(n);
+        int rc = run_reduce(codec, peers, 0, f, false, P, out_codes, nullptr, out_mean, la, s);
         if (rc) return rc;
-        const PeerTable pt = table_of(peers, f, peers.n());
-        const GradArgs fused = {nullptr, nullptr, (uint16_t *)out_codes, out_mean, out_mean};
-        return run_opt(opt, f > 0 ? kSrcPeersFP16Chain : kSrcPeersFP16, kSrcFP16, pl, &pt, fused, gathered, op, x,
-                       m, v, ws, trust_out, s);
+        const PeerTable pt = table_of(peers, f, n);
+        const GradArgs fused = {nullptr, nullptr, (uint16_t *)out_codes, out_mean, out_mean, local_in(la, f, n)};
+        const int src = f > 0 ? kSrcPeersFP16Chain : fused.local.pos >= 0 ? kSrcPeersFP16Local : kSrcPeersFP16;
+        return run_opt(opt, src, kSrcFP16, pl, &pt, fused, gathered, op, x, m, v, ws, trust_out, s);
     }
-    int rc = run_reduce(codec, peers, 0, peers.n(), true, P, out_codes, out_scales, out_mean, s);
+    // int8: the local peer's encode stays a launch of its own (folded into
+    // the reduce it costs more than it saves: the block encode's wave-wide
+    // maximum and divisions lengthen every wave of the reduce)
+    if (la.pos >= 0) {
+        const hipError_t e = timed(K_ENCODE_I8, s, [&] {
+            return launch_encode_i8(la.grad, P, (int8_t *)la.codes, la.scales, s);
+        });
+        if (e != hipSuccess) return hip_fail(e, "encode launch");
+    }
+    int rc = run_reduce(codec, peers, 0, peers.n(), true, P, out_codes, out_scales, out_mean, none, s);
     if (rc) return rc;
     return run_opt(opt, kSrcI8, kSrcI8, pl, nullptr, gathered, gathered, op, x, m, v, ws, trust_out, s);
 }
@@ -538,7 +572,8 @@ int dedloc_reduce_shard(const void *const *peer_codes, const float *const *peer_
         return fail(DEDLOC_ERR_INVALID_ARG, "int8 reduce needs aligned out_scales");
     rc = check_chain(peers, out_mean);
     if (rc) return rc;
-    return run_reduce(codec, peers, 0, peers.n(), true, shard_len, out_codes, out_scales, out_mean,
+    const LocalArgs none = {-1, nullptr, nullptr, nullptr};
+    return run_reduce(codec, peers, 0, peers.n(), true, shard_len, out_codes, out_scales, out_mean, none,
                       (hipStream_t)stream);
 }
 
@@ -567,7 +602,7 @@ int dedloc_lamb_step(float *x, float *m, float *v, const void *grad, const float
     rc = prepare_step(kOptLamb, x, m, v, grad, grad_scales, grad_codec, block, P, offsets, flags, n_tensors,
                       ws, ws_bytes, pl);
     if (rc) return rc;
-    const GradArgs ga = {grad, grad_scales, nullptr, nullptr, nullptr};
+    const GradArgs ga = {grad, grad_scales, nullptr, nullptr, nullptr, {-1, nullptr, nullptr, nullptr}};
     const int src = grad_src(grad_codec);
     return run_opt(kOptLamb, src, src, pl, nullptr, ga, ga, op, x, m, v, ws, trust_out, (hipStream_t)stream);
 }
@@ -583,7 +618,7 @@ int dedloc_lars_step(float *x, float *v, const void *grad, const float *grad_sca
     rc = prepare_step(kOptLars, x, nullptr, v, grad, grad_scales, grad_codec, block, P, offsets, flags,
                       n_tensors, ws, ws_bytes, pl);
     if (rc) return rc;
-    const GradArgs ga = {grad, grad_scales, nullptr, nullptr, nullptr};
+    const GradArgs ga = {grad, grad_scales, nullptr, nullptr, nullptr, {-1, nullptr, nullptr, nullptr}};
     const int src = grad_src(grad_codec);
     return run_opt(kOptLars, src, src, pl, nullptr, ga, ga, op, x, nullptr, v, ws, trust_out, (hipStream_t)stream);
 }
@@ -592,38 +627,40 @@ int dedloc_round(const void *const *peer_codes, const float *const *peer_scales,
                  uint32_t n_peers, const uint64_t *bounds, uint32_t n_shards, int32_t codec, uint32_t block,
                  void *out_codes, float *out_scales, float *x, float *m, float *v, uint64_t P,
                  const uint64_t *offsets, const uint8_t *flags, uint32_t n_tensors,
-                 const dedloc_lamb_cfg *cfg, float *trust_out, float *out_mean, void *ws, size_t ws_bytes,
-                 void *stream) {
+                 const dedloc_lamb_cfg *cfg, float *trust_out, float *out_mean, const dedloc_local_peer *local,
+                 void *ws, size_t ws_bytes, void *stream) {
     OptParams op;
     int rc = lamb_params(cfg, op);
     if (rc) return rc;
     PeerList peers;
     Plan pl;
+    LocalArgs la;
     rc = prepare_round(kOptLamb, peer_codes, peer_scales, counts, n_peers, bounds, n_shards, codec, block,
-                       out_codes, out_scales, x, m, v, P, offsets, flags, n_tensors, out_mean, ws, ws_bytes,
-                       peers, pl);
+                       out_codes, out_scales, x, m, v, P, offsets, flags, n_tensors, out_mean, local, ws, ws_bytes,
+                       peers, pl, la);
     if (rc) return rc;
-    return run_round(kOptLamb, peers, codec, out_codes, out_scales, x, m, v, P, pl, op, trust_out, out_mean, ws,
-                     (hipStream_t)stream);
+    return run_round(kOptLamb, peers, codec, out_codes, out_scales, x, m, v, P, pl, op, trust_out, out_mean, la,
+                     ws, (hipStream_t)stream);
 }
 
 int dedloc_round_lars(const void *const *peer_codes, const float *const *peer_scales, const uint32_t *counts,
                       uint32_t n_peers, const uint64_t *bounds, uint32_t n_shards, int32_t codec,
                       uint32_t block, void *out_codes, float *out_scales, float *x, float *v, uint64_t P,
                       const uint64_t *offsets, const uint8_t *flags, uint32_t n_tensors,
-                      const dedloc_lars_cfg *cfg, float *trust_out, float *out_mean, void *ws,
-                      size_t ws_bytes, void *stream) {
+                      const dedloc_lars_cfg *cfg, float *trust_out, float *out_mean,
+                      const dedloc_local_peer *local, void *ws, size_t ws_bytes, void *stream) {
     OptParams op;
     int rc = lars_params(cfg, op);
     if (rc) return rc;
     PeerList peers;
     Plan pl;
+    LocalArgs la;
     rc = prepare_round(kOptLars, peer_codes, peer_scales, counts, n_peers, bounds, n_shards, codec, block,
-                       out_codes, out_scales, x, nullptr, v, P, offsets, flags, n_tensors, out_mean, ws,
-                       ws_bytes, peers, pl);
+                       out_codes, out_scales, x, nullptr, v, P, offsets, flags, n_tensors, out_mean, local, ws,
+                       ws_bytes, peers, pl, la);
     if (rc) return rc;
     return run_round(kOptLars, peers, codec, out_codes, out_scales, x, nullptr, v, P, pl, op, trust_out, out_mean,
-                     ws, (hipStream_t)stream);
+                     la, ws, (hipStream_t)stream);
 }
 
 size_t dedloc_group_allreduce_workspace_bytes(uint32_t n_peers, uint32_t group_size, uint64_t len,
@@ -680,7 +717,7 @@ int dedloc_group_allreduce(const void *const *peer_codes, const float *const *pe
         if (gt.n_groups == 0) return DEDLOC_OK;
         gt.gbegin[gt.n_groups] = gt.pt.n;
         if (len > 0) {
-            const ChainArgs ca = {nullptr, nullptr, 1};
+            const ChainArgs ca = {nullptr, nullptr, 1, {-1, nullptr, nullptr, nullptr}};
             hipError_t e = codec == DEDLOC_CODEC_FP16
                                ? timed(K_REDUCE_FP16, s, [&] { return launch_reduce_fp16(gt, len, ca, s); })
                                : timed(K_REDUCE_I8, s, [&] { return launch_reduce_i8(gt, len, ca, s); });

@@ -63,13 +63,25 @@ struct GroupTable {
     uint32_t n_groups;
 };
 
+// The local peer of a round: its fp32 gradient is encoded by the pass that
+// averages it (the codes it would have sent are written on the way), at
+// position `pos` of the launch's peer table (-1: no local peer here).
+struct LocalArgs {
+    int32_t pos;
+    const float *grad;  // the full vector, indexed like the messages
+    void *codes;        // its message (output)
+    float *scales;      // int8: its block scales (output)
+};
+
 // A reduce over more peers than one table holds is a chain of launches
 // through an fp32 running sum (stored exactly between launches, so the fma
-// chain is the same as in one pass).  Only a single-group reduce chains.
+// chain is the same as in one pass).  Only a single-group reduce chains, and
+// only a single-group fp16 reduce has a local peer.
 struct ChainArgs {
     const float *acc_in;  // running sum of the peers before this launch (nullable: start at +0)
     float *acc_out;       // the sum after this launch (the mean after the last launch; nullable)
     int final_pass;       // encode into the group outputs
+    LocalArgs local;
 };
 
 // A run of consecutive tensors handled by one LAMB launch (it spans fewer
@@ -105,8 +117,10 @@ enum GradSrc : int {
     kSrcF32 = 0,      // fp32 gradient
     kSrcFP16 = 1,     // fp16 message
     kSrcI8 = 2,       // int8 message + block scales
-    kSrcPeersFP16 = 3,     // fused: average the fp16 peer messages, encode, decode
-    kSrcPeersFP16Chain = 4 // the same, continuing a running sum of earlier peers
+    kSrcPeersFP16 = 3,      // fused: average the fp16 peer messages, encode, decode
+    kSrcPeersFP16Chain = 4, // the same, continuing a running sum of earlier peers (and
+                            // with the local peer if the launch holds it)
+    kSrcPeersFP16Local = 5  // kSrcPeersFP16 with the local peer's encode
 };
 
 struct GradArgs {
@@ -115,6 +129,7 @@ struct GradArgs {
     uint16_t *out_codes;     // kSrcPeersFP16*: gathered encoded average
     float *out_mean;         // kSrcPeersFP16*: fp32 average (nullable)
     const float *acc_in;     // kSrcPeersFP16Chain: running sum of the earlier peers
+    LocalArgs local;         // kSrcPeersFP16Chain / kSrcPeersFP16Local
 };
 
 struct LambWs {

@@ -235,6 +235,35 @@ __device__ __forceinline__ float reduce_fp16_one(const PeerTable &pt, uint32_t p
     return acc;
 }
 
+// Peers [0, n) of the table added to acc, the peer at lp (< n) being the
+// local one: its eight fp32 values are encoded, the codes stored as its
+// message and their decoded values averaged like any peer's.  (Issuing the
+// next peers' loads before the local peer's values are used measured the
+// same, and keeping the local loads inside a peer batch costs registers.)
+__device__ __forceinline__ void reduce_fp16x8_local(const PeerTable &pt, uint32_t n, uint32_t lp,
+                                                    const LocalArgs &la, uint64_t e0, float *acc) {
+    reduce_fp16x8(pt, 0, lp, e0, acc);
+    const f32x4 ga = ld_stream((const f32x4 *)(la.grad + e0)), gb = ld_stream((const f32x4 *)(la.grad + e0 + 4));
+    const float v[8] = {ga[0], ga[1], ga[2], ga[3], gb[0], gb[1], gb[2], gb[3]};
+    const u32x4 lc = pack_fp16x8(v);
+    st_msg((u32x4 *)((uint16_t *)la.codes + e0), lc);
+    float d[8];
+    unpack_fp16x8(lc, d);
+    const float w = pt.w[lp];
+#pragma unroll
+    for (int i = 0; i < 8; i++) acc[i] = fmaf(w, d[i], acc[i]);
+    reduce_fp16x8(pt, lp + 1, n, e0, acc);
+}
+
+__device__ __forceinline__ float reduce_fp16_one_local(const PeerTable &pt, uint32_t n, uint32_t lp,
+                                                       const LocalArgs &la, uint64_t e, float acc) {
+    acc = reduce_fp16_one(pt, 0, lp, e, acc);
+    const unsigned c = f2h(la.grad[e]);
+    ((uint16_t *)la.codes)[e] = (uint16_t)c;
+    acc = fmaf(pt.w[lp], h2f(c), acc);
+    return reduce_fp16_one(pt, lp + 1, n, e, acc);
+}
+
 __global__ __launch_bounds__(kWG) void reduce_fp16_kernel(const GroupTable gt, uint64_t len,
                                                           const ChainArgs ca) {
     const uint32_t g = blockIdx.y;
@@ -243,10 +272,12 @@ __global__ __launch_bounds__(kWG) void reduce_fp16_kernel(const GroupTable gt, u
     uint16_t *__restrict__ out = (uint16_t *)gt.out[g];
     float *mean = ca.acc_out;  // may alias ca.acc_in (same element, same lane)
     const uint64_t e0 = ((uint64_t)blockIdx.x * kWG + threadIdx.x) * kVec;
+    const bool local = ca.local.pos >= 0;  // single group: p_lo = 0
     if (e0 + kVec <= len) {
         float acc[8];
         init8(ca.acc_in, e0, acc);
-        reduce_fp16x8(gt.pt, p_lo, p_hi, e0, acc);
+        if (local) reduce_fp16x8_local(gt.pt, p_hi, ca.local.pos, ca.local, e0, acc);
+        else reduce_fp16x8(gt.pt, p_lo, p_hi, e0, acc);
         if (ca.final_pass) *(u32x4 *)(out + e0) = pack_fp16x8(acc);
         if (mean) {
             *(f32x4 *)(mean + e0) = f32x4{acc[0], acc[1], acc[2], acc[3]};
@@ -254,31 +285,19 @@ __global__ __launch_bounds__(kWG) void reduce_fp16_kernel(const GroupTable gt, u
         }
     } else {
         for (uint64_t e = e0; e < len; e++) {
-            const float a = reduce_fp16_one(gt.pt, p_lo, p_hi, e, ca.acc_in ? ca.acc_in[e] : 0.0f);
+            const float a0 = ca.acc_in ? ca.acc_in[e] : 0.0f;
+            const float a = local ? reduce_fp16_one_local(gt.pt, p_hi, ca.local.pos, ca.local, e, a0)
+                                  : reduce_fp16_one(gt.pt, p_lo, p_hi, e, a0);
             if (ca.final_pass) out[e] = (uint16_t)f2h(a);
             if (mean) mean[e] = a;
         }
     }
 }
 
-// One wave per 1024-element block; lane holds 16 elements.
-__global__ __launch_bounds__(kWG) void reduce_i8_kernel(const GroupTable gt, uint64_t len,
-                                                        const ChainArgs ca) {
-    const uint32_t g = blockIdx.y;
-    const uint32_t p_lo = gt.gbegin[g], p_hi = gt.gbegin[g + 1];
-    if (p_lo == p_hi) return;  // a group without samples produces nothing
-    int8_t *__restrict__ out = (int8_t *)gt.out[g];
-    float *__restrict__ out_scales = gt.out_scales[g];
-    const PeerTable &pt = gt.pt;
-    const uint64_t blk = (uint64_t)blockIdx.x * (kWG / 64) +
-                         (uint64_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    if (blk * kI8Block >= len) return;  // whole wave past the end
-    const uint64_t e0 = blk * kI8Block + (threadIdx.x & 63) * kI8PerLane;
-    const bool full = e0 + kI8PerLane <= len;
-    float *mean = ca.acc_out;  // may alias ca.acc_in (same element, same lane)
-    float acc[kI8PerLane];
-#pragma unroll
-    for (int j = 0; j < kI8PerLane; j++) acc[j] = (ca.acc_in && e0 + j < len) ? ca.acc_in[e0 + j] : 0.0f;
+// Peers [p_lo, p_hi) of the table added to the lane's 16 running sums of
+// block blk (elements e0.., `full` if all 16 are in range).
+__device__ __forceinline__ void reduce_i8_range(const PeerTable &pt, uint32_t p_lo, uint32_t p_hi, uint64_t blk,
+                                                uint64_t e0, uint64_t len, bool full, float *acc) {
     constexpr int B = 4;
     for (uint32_t p0 = p_lo; p0 < p_hi; p0 += B) {
         u32x4 c[B];
@@ -309,6 +328,27 @@ __global__ __launch_bounds__(kWG) void reduce_i8_kernel(const GroupTable gt, uin
             }
         }
     }
+}
+
+// One wave per 1024-element block; lane holds 16 elements.
+__global__ __launch_bounds__(kWG) void reduce_i8_kernel(const GroupTable gt, uint64_t len,
+                                                        const ChainArgs ca) {
+    const uint32_t g = blockIdx.y;
+    const uint32_t p_lo = gt.gbegin[g], p_hi = gt.gbegin[g + 1];
+    if (p_lo == p_hi) return;  // a group without samples produces nothing
+    int8_t *__restrict__ out = (int8_t *)gt.out[g];
+    float *__restrict__ out_scales = gt.out_scales[g];
+    const PeerTable &pt = gt.pt;
+    const uint64_t blk = (uint64_t)blockIdx.x * (kWG / 64) +
+                         (uint64_t)__builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (blk * kI8Block >= len) return;  // whole wave past the end
+    const uint64_t e0 = blk * kI8Block + (threadIdx.x & 63) * kI8PerLane;
+    const bool full = e0 + kI8PerLane <= len;
+    float *mean = ca.acc_out;  // may alias ca.acc_in (same element, same lane)
+    float acc[kI8PerLane];
+#pragma unroll
+    for (int j = 0; j < kI8PerLane; j++) acc[j] = (ca.acc_in && e0 + j < len) ? ca.acc_in[e0 + j] : 0.0f;
+    reduce_i8_range(pt, p_lo, p_hi, blk, e0, len, full, acc);
     if (mean) {
         if (full) {
 #pragma unroll
@@ -372,7 +412,8 @@ __device__ __forceinline__ void load_grad(const GradArgs &ga, const PeerTable &p
         } else {
             float acc[8];
             init8(SRC == kSrcPeersFP16Chain ? ga.acc_in : nullptr, e0, acc);
-            reduce_fp16x8(pt, 0, pt.n, e0, acc);
+            if (SRC != kSrcPeersFP16 && ga.local.pos >= 0) reduce_fp16x8_local(pt, pt.n, ga.local.pos, ga.local, e0, acc);
+            else reduce_fp16x8(pt, 0, pt.n, e0, acc);
             const u32x4 c = pack_fp16x8(acc);
             st_msg((u32x4 *)(ga.out_codes + e0), c);
             if (ga.out_mean) {
@@ -395,7 +436,10 @@ __device__ __forceinline__ void load_grad(const GradArgs &ga, const PeerTable &p
             } else if (SRC == kSrcI8) {
                 g[j] = (float)((const int8_t *)ga.grad)[e] * ga.scales[e / kI8Block];
             } else {
-                const float a = reduce_fp16_one(pt, 0, pt.n, e, SRC == kSrcPeersFP16Chain ? ga.acc_in[e] : 0.0f);
+                const float a0 = SRC == kSrcPeersFP16Chain ? ga.acc_in[e] : 0.0f;
+                const float a = SRC != kSrcPeersFP16 && ga.local.pos >= 0
+                                    ? reduce_fp16_one_local(pt, pt.n, ga.local.pos, ga.local, e, a0)
+                                    : reduce_fp16_one(pt, 0, pt.n, e, a0);
                 const unsigned c = f2h(a);
                 ga.out_codes[e] = (uint16_t)c;
                 if (ga.out_mean) ga.out_mean[e] = a;
@@ -703,6 +747,8 @@ static hipError_t launch_a(int src, const Chunk &ch, uint32_t n_tiles, const Pee
     case kSrcPeersFP16: DEDLOC_LAUNCH(dim3(n_tiles), (opt_a_kernel<kSrcPeersFP16, OPT>), s, ch, p, ga, op, x, m, v, ws);
     case kSrcPeersFP16Chain:
         DEDLOC_LAUNCH(dim3(n_tiles), (opt_a_kernel<kSrcPeersFP16Chain, OPT>), s, ch, p, ga, op, x, m, v, ws);
+    case kSrcPeersFP16Local:
+        DEDLOC_LAUNCH(dim3(n_tiles), (opt_a_kernel<kSrcPeersFP16Local, OPT>), s, ch, p, ga, op, x, m, v, ws);
     default: return hipErrorInvalidValue;
     }
 }

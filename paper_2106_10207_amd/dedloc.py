@@ -70,6 +70,10 @@ def lars_cfg(lr=4.8, momentum=0.9, trust_coef=1e-3, weight_decay=1e-6,
     return dedloc_lars_cfg(lr, momentum, trust_coef, weight_decay, int(force_unit_trust))
 
 
+class dedloc_local_peer(ctypes.Structure):
+    _fields_ = [("index", ctypes.c_uint32), ("grad", ctypes.c_void_p)]
+
+
 class dedloc_balance_problem(ctypes.Structure):
     _fields_ = [("n", ctypes.c_uint32), ("s", ctypes.c_void_p), ("d", ctypes.c_void_p),
                 ("u", ctypes.c_void_p), ("t", ctypes.c_void_p), ("can_aggregate", ctypes.c_void_p),
@@ -101,7 +105,8 @@ _SIGS = {
                       ctypes.c_uint32, ctypes.c_int32, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p,
                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p,
                       ctypes.c_void_p, ctypes.c_uint32, ctypes.POINTER(dedloc_lamb_cfg), ctypes.c_void_p,
-                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p], ctypes.c_int),
+                      ctypes.c_void_p, ctypes.POINTER(dedloc_local_peer), ctypes.c_void_p, ctypes.c_size_t,
+                      ctypes.c_void_p], ctypes.c_int),
     "dedloc_lars_step": ([ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                           ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32,
                           ctypes.POINTER(dedloc_lars_cfg), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
@@ -110,7 +115,8 @@ _SIGS = {
                            ctypes.c_uint32, ctypes.c_int32, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p,
                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p,
                            ctypes.c_void_p, ctypes.c_uint32, ctypes.POINTER(dedloc_lars_cfg), ctypes.c_void_p,
-                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p], ctypes.c_int),
+                           ctypes.c_void_p, ctypes.POINTER(dedloc_local_peer), ctypes.c_void_p, ctypes.c_size_t,
+                           ctypes.c_void_p], ctypes.c_int),
     "dedloc_group_allreduce_workspace_bytes": ([ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int32,
                                                 ctypes.c_uint32], ctypes.c_size_t),
     "dedloc_group_allreduce": ([ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32,
@@ -302,8 +308,11 @@ class RoundCall:
 
     def __init__(self, peer_codes, counts, bounds, codec, out_codes, x, m, v, offsets, flags,
                  cfg, ws, peer_scales=None, out_scales=None, trust_out=None,
-                 out_mean=None, block: int = DEDLOC_I8_BLOCK):
-        self._keep = (peer_codes, peer_scales, out_codes, out_scales, x, m, v, ws, trust_out, out_mean)
+                 out_mean=None, block: int = DEDLOC_I8_BLOCK, local=None):
+        """local: optional (index, fp32 gradient tensor): that peer's message
+        buffers are written by the round (dedloc_local_peer)."""
+        self._keep = (peer_codes, peer_scales, out_codes, out_scales, x, m, v, ws, trust_out, out_mean, local)
+        self.local = None if local is None else ctypes.byref(dedloc_local_peer(int(local[0]), _dev(local[1])))
         self.pc = _ptrs(peer_codes)
         self.ps = None if peer_scales is None else _ptrs(peer_scales)
         self.cnt = _host(counts, np.uint32)
@@ -324,19 +333,21 @@ class RoundCall:
             rc = lib.dedloc_round_lars(self.pc, self.ps, _ptr(self.cnt), len(self.cnt), _ptr(self.bnd),
                                        len(self.bnd) - 1, self.codec, self.block, oc, osc, x, v, P,
                                        _ptr(self.off), _ptr(self.fl), len(self.fl), ctypes.byref(self.cfg),
-                                       tr, om, ws, wsb, _stream(stream))
+                                       tr, om, self.local, ws, wsb, _stream(stream))
         else:
             rc = lib.dedloc_round(self.pc, self.ps, _ptr(self.cnt), len(self.cnt), _ptr(self.bnd),
                                   len(self.bnd) - 1, self.codec, self.block, oc, osc, x, m, v, P,
                                   _ptr(self.off), _ptr(self.fl), len(self.fl), ctypes.byref(self.cfg),
-                                  tr, om, ws, wsb, _stream(stream))
+                                  tr, om, self.local, ws, wsb, _stream(stream))
         _check(rc)
 
 
 def dedloc_round(peer_codes, counts, bounds, codec: int, x, m, v, offsets, flags, cfg: dedloc_lamb_cfg,
                  peer_scales=None, block: int = DEDLOC_I8_BLOCK, out_codes=None, out_scales=None,
-                 trust_out=None, out_mean=None, ws=None, stream=None):
-    """One averaging round; returns (out_codes, out_scales)."""
+                 trust_out=None, out_mean=None, ws=None, stream=None, local=None):
+    """One averaging round; returns (out_codes, out_scales).  local: optional
+    (peer index, fp32 gradient) encoded by the round into that peer's
+    message."""
     import torch
     P = x.numel()
     if out_codes is None:
@@ -346,7 +357,7 @@ def dedloc_round(peer_codes, counts, bounds, codec: int, x, m, v, offsets, flags
     if ws is None:
         ws = make_workspace(P, offsets, x.device)
     RoundCall(peer_codes, counts, bounds, codec, out_codes, x, m, v, offsets, flags, cfg, ws, peer_scales,
-              out_scales, trust_out, out_mean, block)(stream)
+              out_scales, trust_out, out_mean, block, local)(stream)
     return out_codes, out_scales
 
 
@@ -369,7 +380,7 @@ def dedloc_profile_end():
 
 def dedloc_round_lars(peer_codes, counts, bounds, codec: int, x, v, offsets, flags, cfg: dedloc_lars_cfg,
                       peer_scales=None, block: int = DEDLOC_I8_BLOCK, out_codes=None, out_scales=None,
-                      trust_out=None, out_mean=None, ws=None, stream=None):
+                      trust_out=None, out_mean=None, ws=None, stream=None, local=None):
     """One averaging round followed by a LARS step; returns (out_codes, out_scales)."""
     import torch
     P = x.numel()
@@ -380,7 +391,7 @@ def dedloc_round_lars(peer_codes, counts, bounds, codec: int, x, v, offsets, fla
     if ws is None:
         ws = make_workspace(P, offsets, x.device)
     RoundCall(peer_codes, counts, bounds, codec, out_codes, x, None, v, offsets, flags, cfg, ws, peer_scales,
-              out_scales, trust_out, out_mean, block)(stream)
+              out_scales, trust_out, out_mean, block, local)(stream)
     return out_codes, out_scales
 
 

@@ -28,12 +28,14 @@ class DeviceRound:
     sample_ranges: element ranges [a, b) whose fp32 peer gradients are kept
     on the host (for checking against a CPU evaluation of the same inputs).
     poison_zero: zero-sample peers get NaN-filled messages (they must never
-    be read).  fresh: start from m = v = 0."""
+    be read).  fresh: start from m = v = 0.  fused_local: the round itself
+    encodes the local peer's fp32 gradient into its message (the local
+    gradient is kept on the device)."""
 
     def __init__(self, wl: W.Workload, device="cuda", fresh: bool = False,
                  poison_zero: bool = True, step: Optional[int] = None,
                  sample_ranges: Sequence[Tuple[int, int]] = (), keep_local_grad: bool = False,
-                 with_mean: bool = False, optimizer: str = "lamb"):
+                 with_mean: bool = False, optimizer: str = "lamb", fused_local: bool = False):
         import torch
         self.wl = wl
         self.device = device
@@ -63,7 +65,7 @@ class DeviceRound:
                     W.nan_poison(s)
             else:
                 D.dedloc_encode(g, self.codec, self.block or D.DEDLOC_I8_BLOCK, c, s)
-            if p == self.local and keep_local_grad:
+            if p == self.local and (keep_local_grad or fused_local):
                 self.local_grad = g
             del g
             self.codes.append(c)
@@ -85,11 +87,13 @@ class DeviceRound:
             self.v = self.m
         else:
             raise ValueError(f"unknown optimizer {optimizer!r}")
+        self.fused_local = fused_local
         self.call = D.RoundCall(self.codes, self.counts, self.bounds, self.codec, self.out_codes,
                                 self.x, self.m, self.v, self.offsets, self.flags, self.cfg, self.ws,
                                 peer_scales=self.scales if self.codec == D.DEDLOC_CODEC_I8 else None,
                                 out_scales=self.out_scales, trust_out=self.trust, out_mean=self.mean,
-                                block=self.block or D.DEDLOC_I8_BLOCK)
+                                block=self.block or D.DEDLOC_I8_BLOCK,
+                                local=(self.local, self.local_grad) if fused_local else None)
         torch.cuda.synchronize()
 
     def set_step(self, step: int):
@@ -120,3 +124,16 @@ class DeviceRound:
 
     def bytes_encode_local(self) -> float:
         return self.wl.P * (4.0 + self.wl.wire_bytes_per_elem)
+
+    def bytes_step(self) -> float:
+        """Compulsory bytes of one step: the local peer's encode and the
+        round.  With the encode inside the averaging pass, the local message
+        is written but not read back."""
+        b = self.bytes_round() + self.bytes_encode_local()
+        return b - self.wl.P * self.wl.wire_bytes_per_elem if self.local_in_kernel else b
+
+    @property
+    def local_in_kernel(self) -> bool:
+        """The local peer's encode runs inside the averaging pass (the fp16
+        round; the int8 round encodes it in a launch of its own)."""
+        return self.fused_local and self.codec == D.DEDLOC_CODEC_FP16

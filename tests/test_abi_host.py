@@ -162,11 +162,11 @@ def test_round_validation_before_launch():
     pc = (ctypes.c_void_p * 2)(A, A)
     cnt = np.array([1, 1], np.uint32)
 
-    def call(bounds, codec=D.DEDLOC_CODEC_FP16, block=0, ps=None, osc=None):
+    def call(bounds, codec=D.DEDLOC_CODEC_FP16, block=0, ps=None, osc=None, local=None):
         b = np.asarray(bounds, np.uint64)
         return lib.dedloc_round(pc, ps, cnt.ctypes.data, 2, b.ctypes.data, len(b) - 1, codec, block,
                                 A, osc, A, A, A, P, off.ctypes.data, fl.ctypes.data, 2,
-                                ctypes.byref(cfg), None, None, A, need, None)
+                                ctypes.byref(cfg), None, None, local, A, need, None)
     assert call([0, 100, P - 1]) == D.DEDLOC_ERR_INVALID_ARG          # does not end at P
     assert call([0, 3000, 1000, P]) == D.DEDLOC_ERR_INVALID_ARG       # decreasing
     ps = (ctypes.c_void_p * 2)(A, A)
@@ -177,8 +177,17 @@ def test_round_validation_before_launch():
     b = np.array([0, P], np.uint64)
     assert lib.dedloc_round(pc65, None, c65.ctypes.data, 65, b.ctypes.data, 1, D.DEDLOC_CODEC_FP16, 0,
                             A, None, A, A, A, P, off.ctypes.data, fl.ctypes.data, 2,
-                            ctypes.byref(cfg), None, None, A, need, None) == D.DEDLOC_ERR_INVALID_ARG
+                            ctypes.byref(cfg), None, None, None, A, need, None) == D.DEDLOC_ERR_INVALID_ARG
     assert "out_mean" in lib.dedloc_last_error().decode()
+    # the local peer must be a peer with samples and bring an aligned gradient
+    lp = lambda i, g=A: ctypes.byref(D.dedloc_local_peer(i, g))
+    assert call([0, P], local=lp(2)) == D.DEDLOC_ERR_INVALID_ARG
+    assert call([0, P], local=lp(1, A + 4)) == D.DEDLOC_ERR_ALIGN
+    assert call([0, P], local=lp(1, 0)) == D.DEDLOC_ERR_ALIGN
+    cnt[1] = 0
+    assert call([0, P], local=lp(1)) == D.DEDLOC_ERR_INVALID_ARG
+    assert "local" in lib.dedloc_last_error().decode()
+    cnt[1] = 1
 
 
 def _ws_expected(sizes, tile=2048):
