@@ -26,6 +26,9 @@ namespace dedloc {
 #ifndef DEDLOC_TRUST_UNROLL
 #define DEDLOC_TRUST_UNROLL 8   // tile partials loaded per lane before summing
 #endif
+#ifndef DEDLOC_I8_BATCH
+#define DEDLOC_I8_BATCH 16    // int8 peer messages loaded per batch in the reduce
+#endif
 #ifndef DEDLOC_B_REVERSE
 #define DEDLOC_B_REVERSE 1    // pass B visits tiles last-to-first (its re-reads
                               // start with what pass A touched last)

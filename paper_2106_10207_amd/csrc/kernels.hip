@@ -294,39 +294,53 @@ __global__ __launch_bounds__(kWG) void reduce_fp16_kernel(const GroupTable gt, u
     }
 }
 
+// Codes (16 per lane) and block scales of block blk of peers
+// [p0, min(p0 + B, p_hi)); `full` if all 16 elements of the lane are in range.
+__device__ __forceinline__ void load_i8_batch(const PeerTable &pt, uint32_t p0, uint32_t p_hi, uint64_t blk,
+                                              uint64_t e0, uint64_t len, bool full, u32x4 *c, float *s) {
+    constexpr int B = DEDLOC_I8_BATCH;
+#pragma unroll
+    for (int j = 0; j < B; j++) {
+        if (p0 + j < p_hi) {
+            const int8_t *src = (const int8_t *)pt.codes[p0 + j];
+            s[j] = pt.scales[p0 + j][blk];
+            if (full) {
+                c[j] = ld_stream((const u32x4 *)(src + e0));
+            } else {
+                c[j] = u32x4{0u, 0u, 0u, 0u};
+                for (int k = 0; k < kI8PerLane; k++)
+                    if (e0 + k < len) c[j][k >> 2] |= ((unsigned)(uint8_t)src[e0 + k]) << (8 * (k & 3));
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ void fma_i8_batch(const PeerTable &pt, uint32_t p0, uint32_t p_hi, const u32x4 *c,
+                                             const float *s, float *acc) {
+    constexpr int B = DEDLOC_I8_BATCH;
+#pragma unroll
+    for (int j = 0; j < B; j++) {
+        if (p0 + j < p_hi) {
+            const float w = pt.w[p0 + j];
+#pragma unroll
+            for (int k = 0; k < kI8PerLane; k++) {
+                const float d = sbyte(c[j][k >> 2], k & 3) * s[j];
+                acc[k] = fmaf(w, d, acc[k]);
+            }
+        }
+    }
+}
+
 // Peers [p_lo, p_hi) of the table added to the lane's 16 running sums of
-// block blk (elements e0.., `full` if all 16 are in range).
+// block blk (elements e0..).
 __device__ __forceinline__ void reduce_i8_range(const PeerTable &pt, uint32_t p_lo, uint32_t p_hi, uint64_t blk,
                                                 uint64_t e0, uint64_t len, bool full, float *acc) {
-    constexpr int B = 4;
+    constexpr int B = DEDLOC_I8_BATCH;  // peer loads issued before the batch's fmas
     for (uint32_t p0 = p_lo; p0 < p_hi; p0 += B) {
         u32x4 c[B];
         float s[B];
-#pragma unroll
-        for (int j = 0; j < B; j++) {
-            if (p0 + j < p_hi) {
-                const int8_t *src = (const int8_t *)pt.codes[p0 + j];
-                s[j] = pt.scales[p0 + j][blk];
-                if (full) {
-                    c[j] = ld_stream((const u32x4 *)(src + e0));
-                } else {
-                    c[j] = u32x4{0u, 0u, 0u, 0u};
-                    for (int k = 0; k < kI8PerLane; k++)
-                        if (e0 + k < len) c[j][k >> 2] |= ((unsigned)(uint8_t)src[e0 + k]) << (8 * (k & 3));
-                }
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < B; j++) {
-            if (p0 + j < p_hi) {
-                const float w = pt.w[p0 + j];
-#pragma unroll
-                for (int k = 0; k < kI8PerLane; k++) {
-                    const float d = sbyte(c[j][k >> 2], k & 3) * s[j];
-                    acc[k] = fmaf(w, d, acc[k]);
-                }
-            }
-        }
+        load_i8_batch(pt, p0, p_hi, blk, e0, len, full, c, s);
+        fma_i8_batch(pt, p0, p_hi, c, s, acc);
     }
 }
 
