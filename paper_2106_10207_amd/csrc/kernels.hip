@@ -91,9 +91,20 @@ __device__ __forceinline__ void block_sum2(double &a, double &b) {
     __syncthreads();
 }
 
-// Encode one int8 block held by a wave: 16 values per lane, `nvalid` of them
-// real (the rest are zero).  Returns the codes packed in a u32x4 and the
+// Encode one int8 block held by a wave: 16 values per lane (lanes or values
+// past the end hold zero).  Returns the codes packed in a u32x4 and the
 // block scale (same on every lane).
+//
+// The code is rint of the correctly rounded quotient x / s.  It is taken from
+// t = x * rcp(s) instead wherever that provably gives the same integer:
+// v_rcp_f32 is within 1 ulp of 1/s, so |t - x/s| < 1.5 * 2^-23 * |x/s| and
+// |x/s| <= a / fl(a/127) < 127.00001 bound the error by 2.3e-5, and the
+// correctly rounded quotient lies within half an ulp (2^-18 below 128) of
+// x/s.  When t is farther than 2^-14 from every half-integer, x/s, its
+// rounding and t all lie strictly on the same side of every half-integer,
+// so rint(t) is the code.  Lanes holding a value closer to a tie, and blocks
+// whose scale is outside [2^-100, 2^100] (where rcp could leave the normal
+// range), divide.
 __device__ __forceinline__ u32x4 encode_i8_wave(const float *val, float &scale) {
     float a = 0.0f;
 #pragma unroll
@@ -103,11 +114,25 @@ __device__ __forceinline__ u32x4 encode_i8_wave(const float *val, float &scale) 
     scale = (a == 0.0f) ? 0.0f : s;
     u32x4 c = {0u, 0u, 0u, 0u};
     if (a != 0.0f) {
+        float q[kI8PerLane];
+        bool divide = !(s >= 0x1p-100f && s <= 0x1p100f);  // wave-uniform
+        if (!divide) {
+            const float y = __builtin_amdgcn_rcpf(s);
+#pragma unroll
+            for (int j = 0; j < kI8PerLane; j++) {
+                const float t = val[j] * y;
+                q[j] = rintf(t);
+                divide |= fabsf(t - q[j]) > 0.5f - 0x1p-14f;  // t - rint(t) is exact
+            }
+        }
+        if (divide) {
+#pragma unroll
+            for (int j = 0; j < kI8PerLane; j++) q[j] = rintf(val[j] / s);
+        }
 #pragma unroll
         for (int j = 0; j < kI8PerLane; j++) {
-            float q = rintf(val[j] / s);
-            q = fminf(fmaxf(q, -127.0f), 127.0f);
-            c[j >> 2] |= ((unsigned)(int)q & 0xffu) << (8 * (j & 3));
+            const float qc = fminf(fmaxf(q[j], -127.0f), 127.0f);
+            c[j >> 2] |= ((unsigned)(int)qc & 0xffu) << (8 * (j & 3));
         }
     }
     return c;
@@ -141,50 +166,90 @@ __global__ __launch_bounds__(kWG) void decode_fp16_kernel(const uint16_t *__rest
 }
 
 // -------------------------------------------------------------- int8 codec
-// One wave per 1024-element block, 16 elements per lane.
+// One wave per 1024-element block, 16 elements per lane.  In the standalone
+// codec kernels lane l holds elements 256*q + 4*l + r (q, r in 0..3) of its
+// block, so that every 16-byte fp32 access of the wave covers 1 KB without
+// gaps (the block maximum and the per-element codes do not depend on which
+// lane holds which element).
+
+__device__ __forceinline__ uint64_t i8_lane_base(uint64_t blk) { return blk * kI8Block + 4 * (threadIdx.x & 63); }
+#define I8_ELEM(b0, q, r) ((b0) + 256 * (q) + (r))
+
+// The lane's 16 fp32 values of block blk (zero past n).
+__device__ __forceinline__ void load_i8_lane(const float *__restrict__ x, uint64_t n, uint64_t blk, float *val) {
+    const uint64_t b0 = i8_lane_base(blk);
+    if ((blk + 1) * kI8Block <= n) {
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+            const f32x4 a = ld_stream((const f32x4 *)(x + I8_ELEM(b0, q, 0)));
+            val[4 * q] = a[0]; val[4 * q + 1] = a[1]; val[4 * q + 2] = a[2]; val[4 * q + 3] = a[3];
+        }
+    } else {
+#pragma unroll
+        for (int q = 0; q < 4; q++)
+#pragma unroll
+            for (int r = 0; r < 4; r++) {
+                const uint64_t e = I8_ELEM(b0, q, r);
+                val[4 * q + r] = e < n ? x[e] : 0.0f;
+            }
+    }
+}
+
+// Store the lane's 16 codes of block blk (those below n) and the scale.
+__device__ __forceinline__ void store_i8_lane(int8_t *__restrict__ codes, float *__restrict__ scales, uint64_t n,
+                                              uint64_t blk, u32x4 c, float s) {
+    const uint64_t b0 = i8_lane_base(blk);
+    if ((blk + 1) * kI8Block <= n) {
+#pragma unroll
+        // plain stores: with a non-temporal hint the reduce that reads this
+        // message next ran 40 us slower on ALBERT-xlarge
+        for (int q = 0; q < 4; q++) *(unsigned *)(codes + I8_ELEM(b0, q, 0)) = c[q];
+    } else {
+#pragma unroll
+        for (int q = 0; q < 4; q++)
+#pragma unroll
+            for (int r = 0; r < 4; r++) {
+                const uint64_t e = I8_ELEM(b0, q, r);
+                if (e < n) codes[e] = (int8_t)(c[q] >> (8 * r));
+            }
+    }
+    if ((threadIdx.x & 63) == 0) scales[blk] = s;
+}
 
 __global__ __launch_bounds__(kWG) void encode_i8_kernel(const float *__restrict__ x, uint64_t n,
                                                         int8_t *__restrict__ codes,
                                                         float *__restrict__ scales) {
     const uint64_t blk = (uint64_t)blockIdx.x * (kWG / 64) + (threadIdx.x >> 6);
-    const uint64_t e0 = blk * kI8Block + (threadIdx.x & 63) * kI8PerLane;
     if (blk * kI8Block >= n) return;  // whole wave past the end
     float val[kI8PerLane];
-    if (e0 + kI8PerLane <= n) {
-#pragma unroll
-        for (int q = 0; q < 4; q++) {
-            const f32x4 a = ld_stream((const f32x4 *)(x + e0 + 4 * q));
-            val[4 * q] = a[0]; val[4 * q + 1] = a[1]; val[4 * q + 2] = a[2]; val[4 * q + 3] = a[3];
-        }
-    } else {
-#pragma unroll
-        for (int j = 0; j < kI8PerLane; j++) val[j] = (e0 + j < n) ? x[e0 + j] : 0.0f;
-    }
+    load_i8_lane(x, n, blk, val);
     float s;
     const u32x4 c = encode_i8_wave(val, s);
-    if (e0 + kI8PerLane <= n) {
-        *(u32x4 *)(codes + e0) = c;
-    } else {
-        for (int j = 0; j < kI8PerLane; j++)
-            if (e0 + j < n) codes[e0 + j] = (int8_t)(c[j >> 2] >> (8 * (j & 3)));
-    }
-    if ((threadIdx.x & 63) == 0) scales[blk] = s;
+    store_i8_lane(codes, scales, n, blk, c, s);
 }
 
 __global__ __launch_bounds__(kWG) void decode_i8_kernel(const int8_t *__restrict__ codes,
                                                         const float *__restrict__ scales, uint64_t n,
                                                         float *__restrict__ out) {
-    const uint64_t e0 = ((uint64_t)blockIdx.x * kWG + threadIdx.x) * kI8PerLane;
-    if (e0 >= n) return;
-    const float s = scales[e0 / kI8Block];
-    if (e0 + kI8PerLane <= n) {
-        const u32x4 c = *(const u32x4 *)(codes + e0);
+    const uint64_t blk = (uint64_t)blockIdx.x * (kWG / 64) + (threadIdx.x >> 6);
+    if (blk * kI8Block >= n) return;  // whole wave past the end
+    const float s = scales[blk];
+    const uint64_t b0 = i8_lane_base(blk);
+    if ((blk + 1) * kI8Block <= n) {
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+            const unsigned c = *(const unsigned *)(codes + I8_ELEM(b0, q, 0));
+            *(f32x4 *)(out + I8_ELEM(b0, q, 0)) = f32x4{sbyte(c, 0) * s, sbyte(c, 1) * s, sbyte(c, 2) * s,
+                                                        sbyte(c, 3) * s};
+        }
+    } else {
 #pragma unroll
         for (int q = 0; q < 4; q++)
-            *(f32x4 *)(out + e0 + 4 * q) = f32x4{sbyte(c[q], 0) * s, sbyte(c[q], 1) * s,
-                                                 sbyte(c[q], 2) * s, sbyte(c[q], 3) * s};
-    } else {
-        for (uint64_t e = e0; e < n; e++) out[e] = (float)codes[e] * s;
+#pragma unroll
+            for (int r = 0; r < 4; r++) {
+                const uint64_t e = I8_ELEM(b0, q, r);
+                if (e < n) out[e] = (float)codes[e] * s;
+            }
     }
 }
 
@@ -688,22 +753,23 @@ __global__ __launch_bounds__(kWG) void finalize_i8_kernel(float *__restrict__ ac
                                                           int reset) {
     const uint64_t blk = (uint64_t)blockIdx.x * (kWG / 64) + (threadIdx.x >> 6);
     if (blk * kI8Block >= n) return;  // whole wave past the end
-    const uint64_t e0 = blk * kI8Block + (threadIdx.x & 63) * kI8PerLane;
     float val[kI8PerLane];
+    load_i8_lane(acc, n, blk, val);
 #pragma unroll
-    for (int j = 0; j < kI8PerLane; j++) val[j] = (e0 + j < n) ? acc[e0 + j] / count : 0.0f;
+    for (int j = 0; j < kI8PerLane; j++) val[j] = val[j] / count;
     float s;
     const u32x4 c = encode_i8_wave(val, s);
-    if (e0 + kI8PerLane <= n) {
-        *(u32x4 *)(codes + e0) = c;
-    } else {
-        for (int j = 0; j < kI8PerLane; j++)
-            if (e0 + j < n) codes[e0 + j] = (int8_t)(c[j >> 2] >> (8 * (j & 3)));
+    store_i8_lane(codes, scales, n, blk, c, s);
+    if (reset) {
+        const uint64_t b0 = i8_lane_base(blk);
+#pragma unroll
+        for (int q = 0; q < 4; q++)
+#pragma unroll
+            for (int r = 0; r < 4; r++) {
+                const uint64_t e = I8_ELEM(b0, q, r);
+                if (e < n) acc[e] = 0.0f;
+            }
     }
-    if ((threadIdx.x & 63) == 0) scales[blk] = s;
-    if (reset)
-        for (int j = 0; j < kI8PerLane; j++)
-            if (e0 + j < n) acc[e0 + j] = 0.0f;
 }
 
 __global__ __launch_bounds__(kWG) void fill_zero_kernel(uint32_t *p, uint64_t n_words) {
@@ -739,7 +805,7 @@ hipError_t launch_encode_i8(const float *x, uint64_t n, int8_t *codes, float *sc
 
 hipError_t launch_decode_i8(const int8_t *codes, const float *scales, uint64_t n, float *out,
                             hipStream_t s) {
-    DEDLOC_LAUNCH(dim3(grid_for(n, (uint64_t)kWG * kI8PerLane)), decode_i8_kernel, s, codes, scales, n, out);
+    DEDLOC_LAUNCH(dim3(grid_for(n, (uint64_t)kI8Block * (kWG / 64))), decode_i8_kernel, s, codes, scales, n, out);
 }
 
 hipError_t launch_reduce_fp16(const GroupTable &gt, uint64_t len, const ChainArgs &ca, hipStream_t s) {

@@ -88,12 +88,15 @@ class DeviceRound:
         else:
             raise ValueError(f"unknown optimizer {optimizer!r}")
         self.fused_local = fused_local
-        self.call = D.RoundCall(self.codes, self.counts, self.bounds, self.codec, self.out_codes,
-                                self.x, self.m, self.v, self.offsets, self.flags, self.cfg, self.ws,
-                                peer_scales=self.scales if self.codec == D.DEDLOC_CODEC_I8 else None,
-                                out_scales=self.out_scales, trust_out=self.trust, out_mean=self.mean,
-                                block=self.block or D.DEDLOC_I8_BLOCK,
-                                local=(self.local, self.local_grad) if fused_local else None)
+        args = (self.codes, self.counts, self.bounds, self.codec, self.out_codes,
+                self.x, self.m, self.v, self.offsets, self.flags, self.cfg, self.ws)
+        kw = dict(peer_scales=self.scales if self.codec == D.DEDLOC_CODEC_I8 else None,
+                  out_scales=self.out_scales, trust_out=self.trust, out_mean=self.mean,
+                  block=self.block or D.DEDLOC_I8_BLOCK)
+        self.call = D.RoundCall(*args, **kw, local=(self.local, self.local_grad) if fused_local else None)
+        # the round alone, over the messages as they stand (every peer's
+        # message already encoded)
+        self.call_round_only = D.RoundCall(*args, **kw) if fused_local else self.call
         torch.cuda.synchronize()
 
     def set_step(self, step: int):

@@ -96,6 +96,46 @@ def test_encode_decode_i8(n):
     assert np.array_equal(_bits(_np(dec)), _bits(oracle.decode_i8(oc, osc, 1024)))
 
 
+def _near_ties(rng, n_blocks, log_scale):
+    """Blocks whose quotients x / s sit on and within a few ulps of
+    half-integers (where the rounded quotient decides the code), within 1e-3
+    of them (across the distance at which the kernel stops trusting its
+    reciprocal product), or between 2^-13 and 1e-3 from them (where it
+    trusts it); each block keeps its maximum at 10**log_scale."""
+    out = []
+    for b in range(n_blocks):
+        a = np.float32(10.0 ** log_scale[b % len(log_scale)])
+        s = np.float32(a / np.float32(127))
+        k = rng.integers(-127, 127, 1024).astype(np.float64) + 0.5
+        if b % 3 == 1:
+            k += rng.uniform(-1e-3, 1e-3, 1024)
+        elif b % 3 == 2:
+            k += rng.choice([-1.0, 1.0], 1024) * rng.uniform(2.0 ** -13, 1e-3, 1024)
+        x = (k * np.float64(s)).astype(F)
+        step = rng.integers(-3, 4, 1024)
+        for _ in range(3):
+            up, dn = step > 0, step < 0
+            x[up] = np.nextafter(x[up], np.float32(np.inf))
+            x[dn] = np.nextafter(x[dn], np.float32(-np.inf))
+            step = step - np.sign(step)
+        x[rng.integers(0, 1024)] = a if b % 4 < 2 else -a
+        out.append(x)
+    return np.concatenate(out)
+
+
+@pytest.mark.parametrize("log_scale", [[-3.0, 0.0, 2.0], [-37.0, 37.0]], ids=["normal", "extreme"])
+def test_encode_i8_near_ties(log_scale):
+    # codes are rint of the correctly rounded quotient; the kernel takes them
+    # from a reciprocal product only where that provably agrees.  "extreme"
+    # scales (outside [2^-100, 2^100]) always divide.
+    rng = np.random.default_rng(7)
+    x = _near_ties(rng, 96, log_scale)
+    codes, scales = D.dedloc_encode(_up(x), D.DEDLOC_CODEC_I8)
+    oc, osc = oracle.encode_i8(x, 1024)
+    assert np.array_equal(_bits(_np(scales)), _bits(osc))
+    assert np.array_equal(_i8(codes), oc)
+
+
 # --------------------------------------------------------------- reducer
 
 def _peer_messages(codec, n, length, seed, outliers=True):
