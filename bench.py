@@ -64,8 +64,10 @@ KERNEL_KINDS = {
     "dedloc::encode_i8_kernel": "encode_i8",
     "dedloc::decode_fp16_kernel": "decode_fp16",
     "dedloc::decode_i8_kernel": "decode_i8",
-    "dedloc::reduce_fp16_kernel": "reduce_fp16",
-    "dedloc::reduce_i8_kernel": "reduce_i8",
+    "void dedloc::reduce_fp16_kernel<4>": "reduce_fp16",
+    "void dedloc::reduce_fp16_kernel<16>": "reduce_fp16",
+    "void dedloc::reduce_i8_kernel<4>": "reduce_i8",
+    "void dedloc::reduce_i8_kernel<16>": "reduce_i8",
     "void dedloc::opt_a_kernel<0, 0>": "lamb_a_f32",
     "void dedloc::opt_a_kernel<1, 0>": "lamb_a_fp16",
     "void dedloc::opt_a_kernel<2, 0>": "lamb_a_i8",

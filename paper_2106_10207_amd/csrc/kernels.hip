@@ -6,6 +6,8 @@
 // every fused multiply-add is an explicit fmaf, every other operation rounds
 // once, fp32 division and square root are correctly rounded (the HIP
 // defaults), so the results are fixed by the definitions in dedloc.h.
+#include <algorithm>
+
 #include "dedloc_internal.h"
 
 namespace dedloc {
@@ -272,9 +274,9 @@ __device__ __forceinline__ void init8(const float *acc_in, uint64_t e0, float *a
 
 // Eight consecutive fp16 elements starting at e0 (all in range), peers
 // [p_lo, p_hi) of the table, added to the running sums in acc.
+template <int B = kPeerBatch>  // peer loads kept in flight per lane
 __device__ __forceinline__ void reduce_fp16x8(const PeerTable &pt, uint32_t p_lo, uint32_t p_hi,
                                               uint64_t e0, float *acc) {
-    constexpr int B = kPeerBatch;  // peer loads kept in flight per lane
     for (uint32_t p0 = p_lo; p0 < p_hi; p0 += B) {
         u32x4 c[B];
 #pragma unroll
@@ -329,6 +331,10 @@ __device__ __forceinline__ float reduce_fp16_one_local(const PeerTable &pt, uint
     return reduce_fp16_one(pt, lp + 1, n, e, acc);
 }
 
+// B: peer loads per batch (small groups take a small batch, which keeps
+// registers and so more waves in flight).  Only the full batch handles a
+// local peer.
+template <int B>
 __global__ __launch_bounds__(kWG) void reduce_fp16_kernel(const GroupTable gt, uint64_t len,
                                                           const ChainArgs ca) {
     const uint32_t g = blockIdx.y;
@@ -337,12 +343,12 @@ __global__ __launch_bounds__(kWG) void reduce_fp16_kernel(const GroupTable gt, u
     uint16_t *__restrict__ out = (uint16_t *)gt.out[g];
     float *mean = ca.acc_out;  // may alias ca.acc_in (same element, same lane)
     const uint64_t e0 = ((uint64_t)blockIdx.x * kWG + threadIdx.x) * kVec;
-    const bool local = ca.local.pos >= 0;  // single group: p_lo = 0
+    const bool local = B == kPeerBatch && ca.local.pos >= 0;  // single group: p_lo = 0
     if (e0 + kVec <= len) {
         float acc[8];
         init8(ca.acc_in, e0, acc);
         if (local) reduce_fp16x8_local(gt.pt, p_hi, ca.local.pos, ca.local, e0, acc);
-        else reduce_fp16x8(gt.pt, p_lo, p_hi, e0, acc);
+        else reduce_fp16x8<B>(gt.pt, p_lo, p_hi, e0, acc);
         if (ca.final_pass) *(u32x4 *)(out + e0) = pack_fp16x8(acc);
         if (mean) {
             *(f32x4 *)(mean + e0) = f32x4{acc[0], acc[1], acc[2], acc[3]};
@@ -361,9 +367,9 @@ __global__ __launch_bounds__(kWG) void reduce_fp16_kernel(const GroupTable gt, u
 
 // Codes (16 per lane) and block scales of block blk of peers
 // [p0, min(p0 + B, p_hi)); `full` if all 16 elements of the lane are in range.
+template <int B>
 __device__ __forceinline__ void load_i8_batch(const PeerTable &pt, uint32_t p0, uint32_t p_hi, uint64_t blk,
                                               uint64_t e0, uint64_t len, bool full, u32x4 *c, float *s) {
-    constexpr int B = DEDLOC_I8_BATCH;
 #pragma unroll
     for (int j = 0; j < B; j++) {
         if (p0 + j < p_hi) {
@@ -380,9 +386,9 @@ __device__ __forceinline__ void load_i8_batch(const PeerTable &pt, uint32_t p0, 
     }
 }
 
+template <int B>
 __device__ __forceinline__ void fma_i8_batch(const PeerTable &pt, uint32_t p0, uint32_t p_hi, const u32x4 *c,
                                              const float *s, float *acc) {
-    constexpr int B = DEDLOC_I8_BATCH;
 #pragma unroll
     for (int j = 0; j < B; j++) {
         if (p0 + j < p_hi) {
@@ -398,18 +404,20 @@ __device__ __forceinline__ void fma_i8_batch(const PeerTable &pt, uint32_t p0, u
 
 // Peers [p_lo, p_hi) of the table added to the lane's 16 running sums of
 // block blk (elements e0..).
+template <int B>  // peer loads issued before the batch's fmas
 __device__ __forceinline__ void reduce_i8_range(const PeerTable &pt, uint32_t p_lo, uint32_t p_hi, uint64_t blk,
                                                 uint64_t e0, uint64_t len, bool full, float *acc) {
-    constexpr int B = DEDLOC_I8_BATCH;  // peer loads issued before the batch's fmas
     for (uint32_t p0 = p_lo; p0 < p_hi; p0 += B) {
         u32x4 c[B];
         float s[B];
-        load_i8_batch(pt, p0, p_hi, blk, e0, len, full, c, s);
-        fma_i8_batch(pt, p0, p_hi, c, s, acc);
+        load_i8_batch<B>(pt, p0, p_hi, blk, e0, len, full, c, s);
+        fma_i8_batch<B>(pt, p0, p_hi, c, s, acc);
     }
 }
 
-// One wave per 1024-element block; lane holds 16 elements.
+// One wave per 1024-element block; lane holds 16 elements.  B as for
+// reduce_fp16_kernel.
+template <int B>
 __global__ __launch_bounds__(kWG) void reduce_i8_kernel(const GroupTable gt, uint64_t len,
                                                         const ChainArgs ca) {
     const uint32_t g = blockIdx.y;
@@ -427,7 +435,7 @@ __global__ __launch_bounds__(kWG) void reduce_i8_kernel(const GroupTable gt, uin
     float acc[kI8PerLane];
 #pragma unroll
     for (int j = 0; j < kI8PerLane; j++) acc[j] = (ca.acc_in && e0 + j < len) ? ca.acc_in[e0 + j] : 0.0f;
-    reduce_i8_range(pt, p_lo, p_hi, blk, e0, len, full, acc);
+    reduce_i8_range<B>(pt, p_lo, p_hi, blk, e0, len, full, acc);
     if (mean) {
         if (full) {
 #pragma unroll
@@ -808,13 +816,26 @@ hipError_t launch_decode_i8(const int8_t *codes, const float *scales, uint64_t n
     DEDLOC_LAUNCH(dim3(grid_for(n, (uint64_t)kI8Block * (kWG / 64))), decode_i8_kernel, s, codes, scales, n, out);
 }
 
+// Groups of at most this many members take the small peer batch.
+constexpr uint32_t kSmallGroup = 4;
+
+static uint32_t largest_group(const GroupTable &gt) {
+    uint32_t m = 0;
+    for (uint32_t g = 0; g < gt.n_groups; g++) m = std::max(m, gt.gbegin[g + 1] - gt.gbegin[g]);
+    return m;
+}
+
 hipError_t launch_reduce_fp16(const GroupTable &gt, uint64_t len, const ChainArgs &ca, hipStream_t s) {
-    DEDLOC_LAUNCH(dim3(grid_for(len, (uint64_t)kWG * kVec), gt.n_groups), reduce_fp16_kernel, s, gt, len, ca);
+    const dim3 grid(grid_for(len, (uint64_t)kWG * kVec), gt.n_groups);
+    if (ca.local.pos < 0 && largest_group(gt) <= kSmallGroup)
+        DEDLOC_LAUNCH(grid, reduce_fp16_kernel<(int)kSmallGroup>, s, gt, len, ca);
+    DEDLOC_LAUNCH(grid, reduce_fp16_kernel<kPeerBatch>, s, gt, len, ca);
 }
 
 hipError_t launch_reduce_i8(const GroupTable &gt, uint64_t len, const ChainArgs &ca, hipStream_t s) {
-    DEDLOC_LAUNCH(dim3(grid_for(len, (uint64_t)kI8Block * (kWG / 64)), gt.n_groups), reduce_i8_kernel, s, gt, len,
-                  ca);
+    const dim3 grid(grid_for(len, (uint64_t)kI8Block * (kWG / 64)), gt.n_groups);
+    if (largest_group(gt) <= kSmallGroup) DEDLOC_LAUNCH(grid, reduce_i8_kernel<(int)kSmallGroup>, s, gt, len, ca);
+    DEDLOC_LAUNCH(grid, reduce_i8_kernel<DEDLOC_I8_BATCH>, s, gt, len, ca);
 }
 
 template <int OPT>
