@@ -47,7 +47,7 @@ def _parse():
     ap.add_argument("--separate-encode", action="store_true",
                     help="encode the local peer's gradient in its own launch before the round")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-reps", type=int, default=2)
+    ap.add_argument("--cpu-reps", type=int, default=5)
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES, 10 times "
                          "(calibrates HBM byte counters), then exit")
@@ -343,16 +343,27 @@ def cpu_baseline(wl, dr, reps):
             oracle.round_lars(codes, dr.counts, bounds, codec, x, m, wl.offsets(), wl.flags(), cfg,
                               scales or None, 1024)
         times.append(time.perf_counter() - t0)
-    t = float(np.mean(times))
+    t = float(np.median(times))
     return {
         "value": round(dr.bytes_peer_input() / t / 1e9, 4),
         "unit": "GB/s",
         "cores": 1,
         "kind": "oracle",
         "sample": f"the full {wl.name} step (partition + local encode + round over all "
-                  f"{wl.P} elements), mean of {reps} runs, single thread",
+                  f"{wl.P} elements), median of {reps} runs, single thread",
         "s_per_step": round(t, 3),
+        "cpu_model": _cpu_model(),
     }
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def main():
