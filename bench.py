@@ -450,13 +450,17 @@ def main():
     prof = D.dedloc_profile_end()
     kname, roof, per_kernel = kernel_roofline(dr, prof, args.steps)
     roof["traffic"], roof["traffic_source"] = measured_traffic(kname, wl.name)
+    if kname.endswith("fused_fp16") and not dr.local_in_kernel and roof["traffic"] is not None:
+        # the committed counters were taken with the local peer's encode
+        # inside this pass, which moves 4P more bytes
+        roof["traffic"], roof["traffic_source"] = None, roof["traffic_source"] + " (other launch: local encode inside)"
 
     # Back-to-back steps let the 256 MB Infinity Cache keep part of one
     # step's data for the next.  The same steps, each timed alone after
     # reading a 1 GiB buffer (which evicts it with clean lines), give the
     # cold-cache figure.
     flush = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
-    sink = torch.empty(1, device="cuda")
+    sink = torch.empty((), device="cuda")
     evs = []
     for _ in range(args.steps):
         torch.sum(flush, dim=0, out=sink)
