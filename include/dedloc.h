@@ -179,7 +179,9 @@ int dedloc_workspace_clear(void *ws, size_t ws_bytes, void *stream);
  *   flags      host uint8[n_tensors];
  *   trust_out  device float[n_tensors] (nullable): r_t.
  * The norms are accumulated in fp64 in a fixed order, so results are
- * deterministic run to run. */
+ * deterministic run to run.
+ * P = 0 (every tensor empty) is valid: no element is read or written, x,
+ * m, v and grad may be NULL, and trust_out receives r = 1 for every tensor. */
 int dedloc_lamb_step(float *x, float *m, float *v, const void *grad,
                      const float *grad_scales, int32_t grad_codec, uint32_t block,
                      uint64_t P, const uint64_t *offsets, const uint8_t *flags,
@@ -234,7 +236,8 @@ typedef struct {
  *               most 64 peers holding samples, required with more (as in
  *               dedloc_reduce_shard);
  *   local       host, nullable: the local peer (dedloc_local_peer).
- * Workspace as dedloc_lamb_workspace_bytes. */
+ * Workspace as dedloc_lamb_workspace_bytes.  P = 0 is valid as for
+ * dedloc_lamb_step: the messages, outputs and state may then be NULL. */
 int dedloc_round(const void *const *peer_codes, const float *const *peer_scales,
                  const uint32_t *counts, uint32_t n_peers, const uint64_t *bounds,
                  uint32_t n_shards, int32_t codec, uint32_t block, void *out_codes,

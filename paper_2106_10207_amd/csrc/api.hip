@@ -313,8 +313,11 @@ int lars_params(const dedloc_lars_cfg *cfg, OptParams &op) {
 }
 
 // x and the optimizer state (m and v for LAMB, the momentum v for LARS).
-int check_state(int opt, float *x, float *m, float *v, void *ws, size_t ws_bytes, const Plan &pl) {
-    if (!x || !v || (opt == kOptLamb && !m)) return fail(DEDLOC_ERR_INVALID_ARG, "parameter and state buffers must not be NULL");
+// An empty vector (P == 0) reads and writes no element: its buffers may be
+// NULL; only the workspace (the per-tensor ratios) is used.
+int check_state(int opt, float *x, float *m, float *v, uint64_t P, void *ws, size_t ws_bytes, const Plan &pl) {
+    if (P > 0 && (!x || !v || (opt == kOptLamb && !m)))
+        return fail(DEDLOC_ERR_INVALID_ARG, "parameter and state buffers must not be NULL");
     if (!aligned(x, 16) || !aligned(v, 16) || (m && !aligned(m, 16)))
         return fail(DEDLOC_ERR_ALIGN, "parameter and state buffers must be 16-byte aligned");
     if (!ws || ws_bytes < pl.ws_total)
@@ -360,8 +363,9 @@ int prepare_step(int opt, float *x, float *m, float *v, const void *grad, const 
     if (rc) return rc;
     if (!flags) return fail(DEDLOC_ERR_INVALID_ARG, "flags must not be NULL");
     make_plan(P, offsets, flags, n_tensors, pl);
-    rc = check_state(opt, x, m, v, ws, ws_bytes, pl);
+    rc = check_state(opt, x, m, v, P, ws, ws_bytes, pl);
     if (rc) return rc;
+    if (P == 0) return DEDLOC_OK;
     if (!grad || !aligned(grad, 16)) return fail(DEDLOC_ERR_ALIGN, "grad must be non-NULL and 16-byte aligned");
     if (grad_codec == DEDLOC_CODEC_I8 && (!grad_scales || !aligned(grad_scales, 4)))
         return fail(DEDLOC_ERR_INVALID_ARG, "int8 gradient needs aligned grad_scales");
@@ -377,13 +381,13 @@ int prepare_round(int opt, const void *const *peer_codes, const float *const *pe
                   PeerList &peers, Plan &pl, LocalArgs &la) {
     int rc = check_codec(codec, block, false);
     if (rc) return rc;
-    rc = build_peers(peer_codes, peer_scales, counts, n_peers, codec, peers);
+    rc = build_peers(peer_codes, peer_scales, counts, n_peers, codec, peers, P > 0);
     if (rc) return rc;
     la = LocalArgs{-1, nullptr, nullptr, nullptr};
     if (local) {
         if (local->index >= n_peers || counts[local->index] == 0)
             return fail(DEDLOC_ERR_INVALID_ARG, "the local peer must be one of the peers and hold samples");
-        if (!local->grad || !aligned(local->grad, 16))
+        if (P > 0 && (!local->grad || !aligned(local->grad, 16)))
             return fail(DEDLOC_ERR_ALIGN, "the local gradient must be non-NULL and 16-byte aligned");
         for (uint32_t k = 0; k < peers.n(); k++)
             if (peers.index[k] == local->index) la.pos = (int32_t)k;
@@ -402,8 +406,9 @@ int prepare_round(int opt, const void *const *peer_codes, const float *const *pe
     if (rc) return rc;
     if (!flags) return fail(DEDLOC_ERR_INVALID_ARG, "flags must not be NULL");
     make_plan(P, offsets, flags, n_tensors, pl);
-    rc = check_state(opt, x, m, v, ws, ws_bytes, pl);
+    rc = check_state(opt, x, m, v, P, ws, ws_bytes, pl);
     if (rc) return rc;
+    if (P == 0) return DEDLOC_OK;
     if (!out_codes || !aligned(out_codes, 16)) return fail(DEDLOC_ERR_ALIGN, "out_codes must be non-NULL and 16-byte aligned");
     if (out_mean && !aligned(out_mean, 16)) return fail(DEDLOC_ERR_ALIGN, "out_mean must be 16-byte aligned");
     if (codec == DEDLOC_CODEC_I8 && (!out_scales || !aligned(out_scales, 4)))

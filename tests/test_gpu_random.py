@@ -115,10 +115,62 @@ def _case(seed):
 @pytest.mark.parametrize("seed", range(100))
 def test_random_round(seed):
     c = _case(seed)
+    print(f"\n[seed {seed}] codec={c['codec']} opt={c['opt']} P={c['P']} tensors={len(c['flags'])} "
+          f"peers={len(c['counts'])} active={int(np.count_nonzero(c['counts']))} "
+          f"shards={len(c['bounds']) - 1} local={c['local']}", flush=True)
+    _check_round(c)
+
+
+def _degenerate(name, codec, opt):
+    """Edge cases of the round: an empty vector, a vector shorter than one
+    lane's vector, one peer, an empty shard, all-zero gradients (int8 scale
+    0; with m = v = 0 and no weight decay ||u|| = 0, so r = 1), and a lone
+    peer with samples among many without."""
+    rng = np.random.default_rng(len(name) * 7 + codec)
+    sizes, n, counts, local, zero_g, n_shards = [2048], 3, None, None, False, 1
+    if name == "empty":
+        sizes = [0]
+    elif name == "short":
+        sizes, n, local = [5], 1, 0
+    elif name == "empty_shard":
+        sizes, n_shards = [1024 + 3], 4
+    elif name == "zero_grads":
+        sizes, zero_g = [8, 1024, 2048 + 16], True
+    elif name == "lone_peer":
+        n = 40
+        counts = np.zeros(n, np.uint32)
+        counts[17] = 5
+        local = 17
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.uint64)
+    P = int(off[-1])
+    flags = np.full(len(sizes), 2 if zero_g else 3, np.uint8)  # zero_grads: adapt, no decay
+    if counts is None:
+        counts = rng.integers(1, 100, n).astype(np.uint32)
+    grads = [np.zeros(P, F) if zero_g else (rng.standard_normal(P) * 1e-3).astype(F) for _ in range(n)]
+    align = 64 if codec == FP16 else 1024
+    bounds = oracle.partition(P, n_shards, None, align)
+    x = (rng.standard_normal(P) * 0.02).astype(F)
+    m = np.zeros(P, F)
+    v = np.zeros(P, F)
+    if opt == "lamb":
+        cfg = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-6, weight_decay=0.0 if zero_g else 0.01, step=1)
+    else:
+        cfg = dict(lr=4.8, momentum=0.9, trust_coef=1e-3, weight_decay=0.0 if zero_g else 1e-6)
+    return dict(codec=codec, opt=opt, off=off, flags=flags, P=P, counts=counts, local=local, grads=grads,
+                bounds=bounds, x=x, m=m, v=v, cfg=cfg)
+
+
+@pytest.mark.parametrize("name", ["empty", "short", "empty_shard", "zero_grads", "lone_peer"])
+@pytest.mark.parametrize("codec", [FP16, I8])
+@pytest.mark.parametrize("opt", ["lamb", "lars"])
+def test_degenerate_round(name, codec, opt):
+    print(f"\n[{name}] codec={codec} opt={opt}", flush=True)
+    _check_round(_degenerate(name, codec, opt))
+
+
+def _check_round(c):
     codec, P, counts, local = c["codec"], c["P"], c["counts"], c["local"]
     n = len(counts)
-    print(f"\n[seed {seed}] codec={codec} opt={c['opt']} P={P} tensors={len(c['flags'])} peers={n} "
-          f"active={int(np.count_nonzero(counts))} shards={len(c['bounds']) - 1} local={local}", flush=True)
     if codec == FP16:
         codes, scales = [oracle.encode_fp16(g) for g in c["grads"]], None
     else:
