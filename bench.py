@@ -193,7 +193,17 @@ def kernel_roofline(dr, prof, steps):
         "traffic": None,
         "avg_launch_us": round(avg_ms * 1e3, 2),
         "algorithmic_bytes_per_launch": nbytes,
-    }, {k: {"ms_per_step": round(v[0] / steps, 4), "launches_per_step": v[1] / steps} for k, v in prof.items()}
+    }, {k: _kernel_entry(v, steps, per_launch.get(k)) for k, v in prof.items()}
+
+
+def _kernel_entry(v, steps, step_bytes):
+    """ms per step and launches of one kernel kind; with its algorithmic
+    bytes per step (summed over its launches), the achieved GB/s."""
+    total_ms, launches = v
+    e = {"ms_per_step": round(total_ms / steps, 4), "launches_per_step": launches / steps}
+    if step_bytes:
+        e["algorithmic_GBps"] = round(step_bytes / (total_ms / steps * 1e-3) / 1e9, 1)
+    return e
 
 
 def measured_traffic(kernel, workload):
