@@ -114,7 +114,8 @@ int dedloc_weights(const uint32_t *counts, uint32_t n, float *w);
  *         to infinity.  codes: uint16[n].  scales unused (may be NULL).
  *   int8: blocks of `block` elements from x[0] (last block partial):
  *         s = max|x| / 127 (fp32), q = clamp(rint(x/s), -127, 127), ties to
- *         even; an all-zero block has s = 0 and q = 0.  codes: int8[n],
+ *         even; a block with s = 0 (all zero, or max|x| <= 63 * 2^-149 so
+ *         that the division underflows) has every q = 0.  codes: int8[n],
  *         scales: float[ceil(n/block)].  Inputs must be finite.
  * n == 0 is a no-op. */
 int dedloc_encode(const float *x, uint64_t n, int32_t codec, uint32_t block,

@@ -133,9 +133,9 @@ void oracle_decode_fp16(const uint16_t *codes, size_t n, float *out)
 /* 8-bit absmax codec (the build's stress codec).  The message is cut into
  * blocks of `block` elements from its first element; the last block may be
  * partial.  Per block: a = max |x|, s = a / 127 (fp32, correctly rounded);
- * if a == 0 then s = 0 and every code is 0; otherwise
- * q = clamp(rint(x / s), -127, 127) with ties to even.  Decode: x = q * s.
- * Inputs must be finite. */
+ * if s == 0 (a == 0, or a so small that a / 127 underflows: a <= 63 *
+ * 2^-149) every code is 0; otherwise q = clamp(rint(x / s), -127, 127) with
+ * ties to even.  Decode: x = q * s.  Inputs must be finite. */
 void oracle_encode_i8(const float *x, size_t n, uint32_t block, int8_t *codes,
                       float *scales)
 {
@@ -147,11 +147,10 @@ void oracle_encode_i8(const float *x, size_t n, uint32_t block, int8_t *codes,
             if (ax > a) a = ax;
         }
         float s = a / 127.0f;
-        if (a == 0.0f) s = 0.0f;
         scales[bi] = s;
         for (size_t i = b0; i < b1; i++) {
             float q = 0.0f;
-            if (a != 0.0f) {
+            if (s != 0.0f) {
                 q = rintf(x[i] / s);
                 if (q > 127.0f) q = 127.0f;
                 if (q < -127.0f) q = -127.0f;

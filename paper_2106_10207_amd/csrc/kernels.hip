@@ -113,9 +113,9 @@ __device__ __forceinline__ u32x4 encode_i8_wave(const float *val, float &scale) 
     for (int j = 0; j < kI8PerLane; j++) a = fmaxf(a, fabsf(val[j]));
     a = wave_max(a);
     const float s = a / 127.0f;
-    scale = (a == 0.0f) ? 0.0f : s;
+    scale = s;
     u32x4 c = {0u, 0u, 0u, 0u};
-    if (a != 0.0f) {
+    if (s != 0.0f) {  // s == 0: an all-zero block, or a / 127 underflowed; every code is 0
         float q[kI8PerLane];
         bool divide = !(s >= 0x1p-100f && s <= 0x1p100f);  // wave-uniform
         if (!divide) {

@@ -136,6 +136,34 @@ def test_encode_i8_near_ties(log_scale):
     assert np.array_equal(_i8(codes), oc)
 
 
+def test_encode_i8_tiny_blocks():
+    """Blocks at the bottom of the fp32 range: max|x| <= 63 * 2^-149 makes
+    max|x| / 127 underflow to 0 (every code 0), 64 * 2^-149 gives the smallest
+    nonzero scale, and subnormal maxima give subnormal scales.  Also through
+    the reducer and the encode of its average."""
+    tiny = np.float32(2.0 ** -149)
+    rng = np.random.default_rng(11)
+    blocks = []
+    for amax in [1, 2, 63, 64, 65, 127, 128, 1000, 2 ** 20, 2 ** 23, 2 ** 24]:
+        k = rng.integers(-amax, amax + 1, 1024)
+        k[rng.integers(0, 1024)] = amax
+        blocks.append(k.astype(F) * tiny)
+    x = np.concatenate(blocks)
+    codes, scales = D.dedloc_encode(_up(x), D.DEDLOC_CODEC_I8)
+    oc, osc = oracle.encode_i8(x, 1024)
+    assert np.array_equal(_bits(_np(scales)), _bits(osc))
+    assert np.array_equal(_i8(codes), oc)
+    assert osc[0] == 0 and osc[2] == 0 and osc[3] > 0 and not oc[:1024].any()
+    # two peers whose average is that small
+    c2, s2 = oracle.encode_i8(x[::-1].copy(), 1024)
+    counts = np.array([3, 1], np.uint32)
+    rc, rs = D.dedloc_reduce_shard([_up(oc), _up(c2)], counts, x.size, D.DEDLOC_CODEC_I8,
+                                   peer_scales=[_up(osc), _up(s2)])
+    orc, ors, _ = oracle.reduce([oc, c2], counts, oracle.CODEC_I8, [osc, s2], 1024)
+    assert np.array_equal(_bits(_np(rs)), _bits(ors))
+    assert np.array_equal(_i8(rc), orc)
+
+
 # --------------------------------------------------------------- reducer
 
 def _peer_messages(codec, n, length, seed, outliers=True):

@@ -1,0 +1,97 @@
+"""Mutation check of the oracle's pins (CPU only).
+
+Each mutant below is the oracle with one plausible mistake planted in a copy
+of its source: a wrong index, a dropped or sign-flipped term, swapped
+operands, a rounding done twice, an off-by-one in a bound.  Every mutant is
+compiled on its own and the oracle's pin tests (tests/test_oracle_*.py) are
+run against it; the check fails if any mutant passes them all, i.e. if the
+pins would not have noticed that mistake.  The oracle's own source is never
+modified."""
+
+import concurrent.futures
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "dedloc_oracle.c")
+
+# (name, text in the oracle, replacement)
+MUTANTS = [
+    ("partition: share of the wrong peer", "cum += beta ? beta[k - 1] : 1u;", "cum += beta ? beta[k] : 1u;"),
+    ("weights: reciprocal instead of division", "w[p] = (float)counts[p] / (float)W;",
+     "w[p] = (float)counts[p] * (1.0f / (float)W);"),
+    ("fp16: ties away from zero", "if (rem > half || (rem == half && (q & 1))) q++;", "if (rem >= half) q++;"),
+    ("fp16: subnormal shift off by one", "uint64_t r = shift_rne(sig, -e - 1);", "uint64_t r = shift_rne(sig, -e);"),
+    ("fp16: overflow saturates instead of reaching infinity", "if (e > 15) return (uint16_t)(sign | 0x7c00u);",
+     "if (e > 15) return (uint16_t)(sign | 0x7bffu);"),
+    ("int8: scale over 128", "float s = a / 127.0f;", "float s = a / 128.0f;"),
+    ("int8: truncation instead of rounding", "q = rintf(x[i] / s);", "q = truncf(x[i] / s);"),
+    ("int8: clamp at 126", "if (q > 127.0f) q = 127.0f;", "if (q > 126.0f) q = 126.0f;"),
+    ("int8 decode: wrong block", "out[i] = (float)codes[i] * scales[i / block];",
+     "out[i] = (float)codes[i] * scales[(i + 1) / block];"),
+    ("reduce: zero-sample peers read", "if (counts[p] == 0) continue;\n        decode_any", "decode_any"),
+    ("reduce: product and sum rounded separately", "acc[e] = fmaf(w[p], dec[e], acc[e]);",
+     "acc[e] = w[p] * dec[e] + acc[e];"),
+    ("lamb: beta2 in the first moment", "float mn = fmaf(cfg->beta1, m[e], omb1 * gg);",
+     "float mn = fmaf(cfg->beta2, m[e], omb1 * gg);"),
+    ("lamb: first bias correction on v", "float vh = vn / c2;", "float vh = vn / c1;"),
+    ("lamb: eps inside the square root", "float ue = mh / (sqrtf(vh) + cfg->eps) + lam * x[e];",
+     "float ue = mh / sqrtf(vh + cfg->eps) + lam * x[e];"),
+    ("lamb: weight decay sign", "float ue = mh / (sqrtf(vh) + cfg->eps) + lam * x[e];",
+     "float ue = mh / (sqrtf(vh) + cfg->eps) - lam * x[e];"),
+    ("lamb: trust ratio inverted", "r = (float)(X / U);", "r = (float)(U / X);"),
+    ("lamb: update sign", "x[e] = x[e] - lrr * u[e];", "x[e] = x[e] + lrr * u[e];"),
+    ("lamb: decay flag read as the adapt flag", "if (!cfg->force_unit_trust && (flags[t] & 2) && X > 0.0 && U > 0.0)",
+     "if (!cfg->force_unit_trust && (flags[t] & 1) && X > 0.0 && U > 0.0)"),
+    ("lamb: bias correction one step behind", "c1 = (float)(1.0 - pow((double)cfg->beta1, (double)cfg->step));",
+     "c1 = (float)(1.0 - pow((double)cfg->beta1, (double)(cfg->step - 1) + 1e-9));"),
+    ("lars: decay term on the gradient norm", "r = (float)((double)cfg->trust_coef * X / (G + (double)lam * X));",
+     "r = (float)((double)cfg->trust_coef * X / (G + (double)lam * G));"),
+    ("lars: decay dropped from the step", "float d = g[e] + lam * x[e];", "float d = g[e];"),
+    ("lars: momentum on the step", "float vn = fmaf(cfg->momentum, v[e], s * d);",
+     "float vn = fmaf(cfg->momentum, s * d, v[e]);"),
+    ("round: shard offset in elements, not bytes", "pc[p] = (const char *)peer_codes[p] + b0 * cb;",
+     "pc[p] = (const char *)peer_codes[p] + b0;"),
+    ("group: digit stride", "const uint32_t base = (g / lo) * lo * m + (g % lo);",
+     "const uint32_t base = (g / lo) * m + (g % lo);"),
+    ("group: a member counted once per group", "ncnt[s] = gt;", "ncnt[s] = cnt[s];"),
+    ("accumulate: batch size dropped", "acc[i] = fmaf(b, gi, acc[i]);", "acc[i] = acc[i] + gi;"),
+    ("finalize: reciprocal instead of division", "scratch[i] = acc[i] / c;", "scratch[i] = acc[i] * (1.0f / c);"),
+]
+
+
+def _pins_on(lib_path):
+    code = ("import sys, oracle\n"
+            f"oracle._LIB = {lib_path!r}\n"
+            "import pytest, glob\n"
+            "files = sorted(glob.glob('tests/test_oracle_*.py'))\n"
+            f"files = [f for f in files if not f.endswith({os.path.basename(__file__)!r})]\n"
+            "sys.exit(pytest.main(['-x', '-q', '-p', 'no:cacheprovider', '-m', 'not gpu'] + files))\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True, timeout=600)
+    return r.returncode
+
+
+def _mutant(i, name, old, new, tmp):
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation site not unique or missing: {name}"
+    c = os.path.join(tmp, f"mutant_{i}.c")
+    lib = os.path.join(tmp, f"liboracle_mutant_{i}.so")
+    open(c, "w").write(src.replace(old, new))
+    subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math",
+                           c, "-o", lib, "-lm"])
+    return name, _pins_on(lib)
+
+
+def test_pins_catch_every_mutant(tmp_path):
+    assert _pins_on(os.path.join(ROOT, "oracle", "liboracle.so")) == 0  # the real oracle passes
+    with concurrent.futures.ThreadPoolExecutor(max_workers=4) as ex:
+        results = list(ex.map(lambda a: _mutant(a[0], *a[1], str(tmp_path)), enumerate(MUTANTS)))
+    survivors = [name for name, rc in results if rc == 0]
+    assert not survivors, f"mutants the pins do not catch: {survivors}"
+
+
+if __name__ == "__main__":
+    pytest.main([__file__, "-q"])

@@ -7,7 +7,8 @@ extreme magnitudes, ties, zero and repeated values).
   conversion, an independent implementation, agrees bit for bit.
 * int8 absmax, per block of 1024: s = fl(max|x| / 127); the element that
   attains the maximum codes to +-127; |x - q*s| <= s/2 plus the rounding of
-  the quotient and of the product; an all-zero block has s = 0 and codes 0.
+  the quotient and of the product while s is a normal number; a block with
+  s = 0 (all zero, or max|x| / 127 underflowing) has codes 0.
 * Shard bounds: the closed form with exact integers (Python's unbounded
   ints), which tile [0, P) in order, each interior bound a multiple of the
   alignment.
@@ -20,7 +21,7 @@ extreme magnitudes, ties, zero and repeated values).
 from fractions import Fraction
 
 import numpy as np
-from hypothesis import HealthCheck, given, settings
+from hypothesis import HealthCheck, example, given, settings
 from hypothesis import strategies as st
 from hypothesis.extra import numpy as hnp
 
@@ -82,8 +83,15 @@ block_values = hnp.arrays(np.float32, st.integers(1, 2600),
                           elements=st.floats(-2.0 ** 100, 2.0 ** 100, width=32, allow_nan=False))
 
 
+TINY = 2.0 ** -149  # the smallest fp32 subnormal
+
+
 @SETTINGS
 @given(block_values)
+@example(np.array([TINY], np.float32))                          # a / 127 underflows: s = 0
+@example(np.array([63 * TINY, -TINY, 0.0], np.float32))         # the largest block with s = 0
+@example(np.array([64 * TINY, 3 * TINY, -64 * TINY], np.float32))  # the smallest nonzero scale
+@example(np.array([1e-40, -3e-41, 2e-42], np.float32))          # subnormal scale
 def test_int8_codec_properties(x):
     codes, scales = oracle.encode_i8(x, 1024)
     dec = oracle.decode_i8(codes, scales, 1024)
@@ -94,16 +102,22 @@ def test_int8_codec_properties(x):
         a = float(np.max(np.abs(blk)))
         s = float(scales[b])
         assert s == float(np.float32(np.float32(a) / np.float32(127.0)))
-        if a == 0.0:
-            assert s == 0.0 and not q.any()
+        if s == 0.0:  # all zero, or a / 127 below half the smallest subnormal
+            assert a <= 63 * TINY and not q.any()
             continue
         assert np.all(np.abs(q) <= 127)
         i = int(np.argmax(np.abs(blk)))
-        assert abs(int(q[i])) == 127 and np.sign(q[i]) == np.sign(blk[i])
+        assert q[i] != 0 and np.sign(q[i]) == np.sign(blk[i])
         err = np.abs(blk - dec[b * 1024:(b + 1) * 1024].astype(np.float64))
-        # half a step, plus the rounding of x/s (half an ulp below 128 -> 2^-17
-        # of a step) and of q*s (half an fp32 ulp of the value)
-        bound = s / 2 * (1 + 2.0 ** -16) + np.abs(blk) * 2.0 ** -23 + 1e-45
+        if s >= 2.0 ** -126:
+            assert abs(int(q[i])) == 127  # a / s rounds to 127 when s is normal
+            # half a step, plus the rounding of x/s (half an ulp below 128 ->
+            # 2^-17 of a step) and of q*s (half an fp32 ulp of the value)
+            bound = s / 2 * (1 + 2.0 ** -16) + np.abs(blk) * 2.0 ** -23 + TINY
+        else:
+            # a subnormal scale carries few significant bits, so a / s may
+            # exceed 127 and the clamp may cost more than half a step
+            bound = np.full(blk.shape, a + s)
         assert np.all(err <= bound)
 
 
