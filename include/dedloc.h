@@ -111,7 +111,8 @@ int dedloc_weights(const uint32_t *counts, uint32_t n, float *w);
 
 /* Encode n fp32 values (the sender's side of the exchange).
  *   fp16: IEEE binary16, round to nearest even, subnormals kept, overflow
- *         to infinity.  codes: uint16[n].  scales unused (may be NULL).
+ *         to infinity, NaN to a NaN of the same sign (payload unspecified).
+ *         codes: uint16[n].  scales unused (may be NULL).
  *   int8: blocks of `block` elements from x[0] (last block partial):
  *         s = max|x| / 127 (fp32), q = clamp(rint(x/s), -127, 127), ties to
  *         even; a block with s = 0 (all zero, or max|x| <= 63 * 2^-149 so

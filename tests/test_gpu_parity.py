@@ -74,6 +74,20 @@ def test_encode_fp16(n):
     assert np.array_equal(_u16(codes), oracle.encode_fp16(x))
 
 
+def test_encode_fp16_nan():
+    """A NaN encodes to a NaN of the same sign (the payload is not part of
+    the definition); the oracle's and the kernel's may differ in it."""
+    x = np.array([np.nan, -np.nan, 1.0, np.float32(np.nan) * 0], F)
+    x.view(np.uint32)[0] = 0x7fc01234  # a quiet NaN with a payload
+    x.view(np.uint32)[3] = 0xff800001  # a signalling NaN
+    g = _u16(D.dedloc_encode(_up(x), D.DEDLOC_CODEC_FP16)[0])
+    o = oracle.encode_fp16(x)
+    for i in (0, 1, 3):
+        assert (g[i] & 0x7c00) == 0x7c00 and (g[i] & 0x3ff) != 0, hex(g[i])
+        assert (g[i] & 0x8000) == (o[i] & 0x8000) and (o[i] & 0x7fff) > 0x7c00
+    assert g[2] == o[2]
+
+
 def test_decode_fp16_all_patterns():
     h = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
     out = D.dedloc_decode(_up(h.view(np.int16)), None, h.size, D.DEDLOC_CODEC_FP16)
