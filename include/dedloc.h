@@ -143,6 +143,10 @@ int dedloc_decode(const void *codes, const float *scales, uint64_t n,
  * peers holding samples, required with more (it then carries the running
  * sum between launches, stored exactly, so the result is the same as one
  * pass).
+ * Non-finite fp16 codes (a sender whose gradient overflowed) are averaged
+ * like any other value: an element with an infinity from one peer averages
+ * to that infinity, +inf meeting -inf or a NaN code gives NaN, and the NaN
+ * is encoded with either sign.  int8 scales must be finite.
  * Errors: n_peers == 0 or > DEDLOC_MAX_PEERS -> INVALID_ARG; all counts
  * zero -> ZERO_WEIGHT; more than 64 peers with samples and out_mean NULL ->
  * INVALID_ARG.  shard_len == 0 is a no-op (after validation). */
@@ -181,7 +185,10 @@ int dedloc_workspace_clear(void *ws, size_t ws_bytes, void *stream);
  *   flags      host uint8[n_tensors];
  *   trust_out  device float[n_tensors] (nullable): r_t.
  * The norms are accumulated in fp64 in a fixed order, so results are
- * deterministic run to run.
+ * deterministic run to run.  Non-finite gradient values are neither skipped
+ * nor clamped: they go through the formulas above.  r_t is the quotient
+ * only when both norms compare greater than 0, so a NaN norm gives r_t = 1;
+ * an infinite norm gives 0 or infinity by the division.
  * P = 0 (every tensor empty) is valid: no element is read or written, x,
  * m, v and grad may be NULL, and trust_out receives r = 1 for every tensor. */
 int dedloc_lamb_step(float *x, float *m, float *v, const void *grad,

@@ -48,6 +48,10 @@ MUTANTS = [
      "if (!cfg->force_unit_trust && (flags[t] & 1) && X > 0.0 && U > 0.0)"),
     ("lamb: bias correction one step behind", "c1 = (float)(1.0 - pow((double)cfg->beta1, (double)cfg->step));",
      "c1 = (float)(1.0 - pow((double)cfg->beta1, (double)(cfg->step - 1) + 1e-9));"),
+    ("lamb: NaN norms pass the zero rule", "if (!cfg->force_unit_trust && (flags[t] & 2) && X > 0.0 && U > 0.0)",
+     "if (!cfg->force_unit_trust && (flags[t] & 2) && X != 0.0 && U != 0.0)"),
+    ("lars: NaN norms pass the zero rule", "if (!cfg->force_unit_trust && (flags[t] & 2) && X > 0.0 && G > 0.0)",
+     "if (!cfg->force_unit_trust && (flags[t] & 2) && X != 0.0 && G != 0.0)"),
     ("lars: decay term on the gradient norm", "r = (float)((double)cfg->trust_coef * X / (G + (double)lam * X));",
      "r = (float)((double)cfg->trust_coef * X / (G + (double)lam * G));"),
     ("lars: decay dropped from the step", "float d = g[e] + lam * x[e];", "float d = g[e];"),
