@@ -88,6 +88,71 @@ def test_encode_fp16_nan():
     assert g[2] == o[2]
 
 
+def _fp16_boundaries():
+    """Every fp32 value at which binary16 rounding can go wrong: each finite
+    fp16 value and its fp32 neighbours, each midpoint between consecutive
+    fp16 values (a tie) and its fp32 neighbours, the overflow threshold
+    65520 and its neighbours, both signs."""
+    h = np.arange(0x7C00, dtype=np.uint16)
+    v = h.view(np.float16).astype(F)
+    mid = ((v[:-1].astype(np.float64) + v[1:].astype(np.float64)) / 2).astype(F)  # exact in fp32
+    mid = np.concatenate([mid, [F(65520.0)]])
+    base = np.concatenate([v, mid])
+    up = np.nextafter(base, F(np.inf))
+    dn = np.nextafter(base, F(-np.inf))
+    pos = np.concatenate([base, up, dn])
+    return np.concatenate([pos, -pos]).astype(F)
+
+
+def test_encode_fp16_every_boundary():
+    x = _fp16_boundaries()
+    codes, _ = D.dedloc_encode(_up(x), D.DEDLOC_CODEC_FP16)
+    assert np.array_equal(_u16(codes), oracle.encode_fp16(x))
+
+
+def test_round_fp16_encodes_every_boundary():
+    """The round's own fp16 encodes: the local peer's fp32 gradient (encoded
+    inside the pass that averages it) holds every boundary value, and two
+    peers of equal counts whose codes are consecutive fp16 values make every
+    average an exact tie, which the re-encode must round to even."""
+    x_all = _fp16_boundaries()
+    x_all = x_all[np.abs(x_all) < 65504]  # keep the optimizer's state finite
+    P = x_all.size
+    h = np.arange(0x7BFF, dtype=np.uint16)
+    lo = np.resize(np.concatenate([h, h | 0x8000]), P)
+    hi = (lo + 1).astype(np.uint16)  # the next magnitude, same sign
+    rng = np.random.default_rng(3)
+    codes = [lo, hi, oracle.encode_fp16(x_all)]
+    counts = np.array([4, 4, 0], np.uint32)
+    off, flags = np.array([0, P], np.uint64), np.array([3], np.uint8)
+    x = (rng.standard_normal(P) * 0.02).astype(F)
+    m, v = np.zeros(P, F), np.zeros(P, F)
+    cfg = dict(lr=1e-3, weight_decay=0.01, step=1)
+    bounds = oracle.partition(P, 2, None, 64)
+    for local in (None, 2):
+        cnt = counts.copy()
+        if local is not None:
+            cnt[2] = 1
+        dc = [_up(c.view(np.int16)) for c in codes]
+        if local is not None:
+            W.nan_poison(dc[local])
+        xd, md, vd = _up(x), _up(m), _up(v)
+        mean = torch.empty(P, dtype=torch.float32, device=DEV)
+        loc = None if local is None else (local, _up(x_all))
+        oc, _ = D.dedloc_round(dc, cnt, bounds, D.DEDLOC_CODEC_FP16, xd, md, vd, off, flags,
+                               D.lamb_cfg(**cfg), out_mean=mean, local=loc)
+        r = oracle.round_(codes, cnt, bounds, oracle.CODEC_FP16, x, m, v, off, flags, oracle.lamb_cfg(**cfg))
+        if local is None:  # the two peers' averages are exact ties
+            assert np.array_equal(r["mean"].astype(np.float64),
+                                  (lo.view(np.float16).astype(np.float64) + hi.view(np.float16)) / 2)
+        else:
+            assert np.array_equal(_u16(dc[local]), codes[local])
+        assert np.array_equal(_bits(_np(mean)), _bits(r["mean"]))
+        assert np.array_equal(_u16(oc), r["codes"])
+        assert np.array_equal(_bits(_np(md)), _bits(r["m"]))
+        _assert_x(_np(xd), r["x"], x)
+
+
 def test_decode_fp16_all_patterns():
     h = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
     out = D.dedloc_decode(_up(h.view(np.int16)), None, h.size, D.DEDLOC_CODEC_FP16)
