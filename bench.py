@@ -363,6 +363,7 @@ def cpu_baseline(wl, dr, reps):
                   f"{wl.P} elements), median of {reps} runs, single thread",
         "s_per_step": round(t, 3),
         "cpu_model": _cpu_model(),
+        "host_threads_available": len(os.sched_getaffinity(0)),
     }
 
 
