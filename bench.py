@@ -35,11 +35,14 @@ def _parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="albert_large")
-    ap.add_argument("--mode", default="round", choices=["round", "group", "balance"],
+    ap.add_argument("--mode", default="round", choices=["round", "group", "balance", "accumulate"],
                     help="round: the averaging round (default); group: the group (Moshpit) "
                          "all-reduce of the workload's peer messages; balance: host solve time of "
-                         "the load-balancing LP for 4..32 peers")
+                         "the load-balancing LP for 4..32 peers; accumulate: the local peer's "
+                         "gradient accumulation and its overlap with the round")
     ap.add_argument("--group-size", type=int, default=8)
+    ap.add_argument("--micro", type=int, default=8,
+                    help="accumulate mode: micro-batches accumulated per round")
     ap.add_argument("--graph", action="store_true",
                     help="capture one step (encode + round) in a HIP graph and time its replays")
     ap.add_argument("--optimizer", default="lamb", choices=["lamb", "lars"],
@@ -311,6 +314,124 @@ def bench_group(args, wl):
     }
 
 
+def _event_ms(fn, reps, stream=None):
+    """Average ms of fn() over reps back-to-back calls, timed with HIP events
+    on `stream` (torch's current stream by default)."""
+    import torch
+    s = stream or torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(s)
+    for _ in range(reps):
+        fn()
+    e1.record(s)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def bench_accumulate(args, wl):
+    """Local accumulation (Section 3.1: a peer accumulates micro-batch
+    gradients until the collaboration reaches its target batch).  A step adds
+    --micro micro-batches of 32 samples into the fp32 accumulator
+    (dedloc_accumulate), then turns it into the peer's message
+    (dedloc_finalize, which also zeroes the accumulator).  Algorithmic bytes
+    per element: accumulate 12 (fp32 gradient: acc read and written, gradient
+    read) or 10 (fp16 codes); finalize 8 + b (acc read and zeroed, message
+    written).  The overlap case runs the workload's round on the current
+    stream while the next step's accumulation runs on a second stream
+    (Section 3.2's delayed update), against the two one after the other."""
+    import torch
+    from paper_2106_10207_amd import dedloc as D
+    from paper_2106_10207_amd import harness as H
+    dr = H.DeviceRound(wl, "cuda", keep_local_grad=True, fused_local=True)
+    P = wl.P
+    k = args.micro
+    acc = torch.zeros(P, dtype=torch.float32, device="cuda")
+    g32 = dr.local_grad
+    g16 = D.dedloc_encode(g32, D.DEDLOC_CODEC_FP16)[0]
+    msg, msg_scales = D.dedloc_finalize(acc, 1, dr.codec, reset=False)
+
+    def acc32():
+        D.dedloc_accumulate(acc, g32, 32.0)
+
+    def acc16():
+        D.dedloc_accumulate(acc, g16, 32.0)
+
+    def fin():
+        D.dedloc_finalize(acc, 32 * k, dr.codec, codes=msg, scales=msg_scales, reset=True)
+
+    def accumulate_step(stream=None):
+        with torch.cuda.stream(stream or torch.cuda.current_stream()):
+            for _ in range(k):
+                acc32()
+            fin()
+
+    reps = max(args.steps, 1)
+    for fn in (acc32, acc16, fin, accumulate_step, dr.run):
+        for _ in range(args.warmup):
+            fn()
+    t_acc32 = _event_ms(acc32, reps * k)
+    t_acc16 = _event_ms(acc16, reps * k)
+    t_fin = _event_ms(fin, reps)
+    t_step = _event_ms(accumulate_step, reps)
+    t_round = _event_ms(dr.run, reps)
+
+    side = torch.cuda.Stream()  # default priority
+
+    def serial():
+        dr.run()
+        accumulate_step()
+
+    def overlapped():
+        main = torch.cuda.current_stream()
+        side.wait_stream(main)
+        accumulate_step(side)
+        dr.run()
+        main.wait_stream(side)
+
+    for _ in range(args.warmup):
+        serial()
+        overlapped()
+    t_serial = _event_ms(serial, reps)
+    t_overlap = _event_ms(overlapped, reps)
+
+    # per-launch events of the library's own profiler for the roofline
+    D.dedloc_profile_begin(4 * reps * (k + 1) + 64)
+    for _ in range(reps):
+        for _ in range(k):
+            acc32()
+        fin()
+    prof = D.dedloc_profile_end()
+    b = wl.wire_bytes_per_elem
+    acc_ms = prof["accumulate"][0] / prof["accumulate"][1]
+    fin_kind = "finalize_fp16" if dr.codec == D.DEDLOC_CODEC_FP16 else "finalize_i8"
+    fin_ms = prof[fin_kind][0] / prof[fin_kind][1]
+
+    def gbps(nbytes, ms):
+        return round(nbytes / (ms * 1e-3) / 1e9, 1)
+
+    acc_bytes = 12.0 * P
+    return {
+        "metric": "local gradient accumulation, algorithmic GB/s of the accumulate kernel",
+        "value": gbps(acc_bytes, t_acc32), "unit": "GB/s", "n_gpus": 1, "steps": reps,
+        "warmup": args.warmup, "ms_per_step": round(t_step, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "mode": "accumulate", "params": P, "micro_batches": k,
+                   "wire": wl.codec},
+        "accumulate_fp32": {"ms": round(t_acc32, 5), "GBps": gbps(acc_bytes, t_acc32)},
+        "accumulate_fp16": {"ms": round(t_acc16, 5), "GBps": gbps(10.0 * P, t_acc16)},
+        "finalize": {"ms": round(t_fin, 5), "GBps": gbps((8.0 + b) * P, t_fin)},
+        "overlap": {"round_ms": round(t_round, 5), "accumulate_step_ms": round(t_step, 5),
+                    "serial_ms": round(t_serial, 5), "overlapped_ms": round(t_overlap, 5)},
+        "roofline": {"bound": "hbm", "kernel": "accumulate", "achieved": gbps(acc_bytes, acc_ms),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(acc_bytes / (acc_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "avg_launch_us": round(acc_ms * 1e3, 2), "algorithmic_bytes_per_launch": acc_bytes,
+                     "finalize_avg_launch_us": round(fin_ms * 1e3, 2),
+                     "finalize_GBps": gbps((8.0 + b) * P, fin_ms)},
+    }
+
+
 def cpu_baseline(wl, dr, reps):
     """The oracle (plain sequential C) on the same workload: one local encode
     plus one round, on the host, timed after its inputs are prepared."""
@@ -411,6 +532,9 @@ def main():
     D.load()
     if args.mode == "group":
         print(json.dumps(bench_group(args, wl)), flush=True)
+        return
+    if args.mode == "accumulate":
+        print(json.dumps(bench_accumulate(args, wl)), flush=True)
         return
     dr = H.DeviceRound(wl, "cuda", keep_local_grad=True, optimizer=args.optimizer,
                        fused_local=not args.separate_encode)
