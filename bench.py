@@ -89,20 +89,27 @@ KERNEL_KINDS = {
     "void dedloc::opt_b_kernel<0, 1>": "lars_b",
     "void dedloc::opt_b_kernel<1, 1>": "lars_b",
     "void dedloc::opt_b_kernel<2, 1>": "lars_b",
+    "void dedloc::accumulate_kernel<false>": "accumulate",
+    "void dedloc::accumulate_kernel<true>": "accumulate_fp16",
+    "dedloc::finalize_fp16_kernel": "finalize_fp16",
+    "dedloc::finalize_i8_kernel": "finalize_i8",
 }
+# kernels whose counters come from the accumulate mode (the other kinds from the round)
+ACCUMULATE_KINDS = ("accumulate", "accumulate_fp16", "finalize_fp16", "finalize_i8")
 
 COUNTER_COMMANDS = (
     "timeout -s KILL 120 rocprofv3 --pmc {c} --output-format csv -d DIR/pmc_{c} -o run -- "
-    "python3 bench.py --workload {w} --steps 5 --warmup 1 --no-cpu-baseline",
+    "python3 bench.py --mode {m} --workload {w} --steps 5 --warmup 1 --no-cpu-baseline",
     "timeout -s KILL 60 rocprofv3 --pmc {c} --output-format csv -d DIR/pmc_copy_{c} -o run -- "
     "python3 bench.py --copy-probe 268435456",
 )
 
 
-def summarize_counters(root_dir, workload):
+def summarize_counters(root_dir, workload, mode="round"):
     """Per-kernel HBM bytes per launch from FETCH_SIZE and WRITE_SIZE (KiB per
     dispatch), each scaled by the ratio of known bytes to the counter's
-    reading for a plain 256 MiB device copy."""
+    reading for a plain 256 MiB device copy.  Counters taken in `mode` give
+    the records of that mode's own kernels only."""
     import csv
     import hashlib
     from collections import defaultdict
@@ -125,7 +132,7 @@ def summarize_counters(root_dir, workload):
                                  "rb").read()).hexdigest()
     written = []
     for name, kind in KERNEL_KINDS.items():
-        if name not in fetch or name not in write:
+        if name not in fetch or name not in write or (kind in ACCUMULATE_KINDS) != (mode == "accumulate"):
             continue
         fb = fetch[name] * 1024.0 * scale["FETCH_SIZE"]
         wb = write[name] * 1024.0 * scale["WRITE_SIZE"]
@@ -135,7 +142,8 @@ def summarize_counters(root_dir, workload):
             "copy_calibration": {"bytes": copy_bytes, "fetch_scale": scale["FETCH_SIZE"],
                                  "write_scale": scale["WRITE_SIZE"]},
             "hbm_bytes_per_launch": fb + wb, "read_bytes_per_launch": fb, "write_bytes_per_launch": wb,
-            "commands": [c.format(c=k, w=workload) for c in COUNTER_COMMANDS for k in ("FETCH_SIZE", "WRITE_SIZE")],
+            "commands": [c.format(c=k, w=workload, m=mode) for c in COUNTER_COMMANDS
+                         for k in ("FETCH_SIZE", "WRITE_SIZE")],
             "kernels_hip_sha256": digest,
         }
         out = os.path.join(root, "profiles", f"traffic_{kind}_{workload}.json")
@@ -411,6 +419,7 @@ def bench_accumulate(args, wl):
         return round(nbytes / (ms * 1e-3) / 1e9, 1)
 
     acc_bytes = 12.0 * P
+    traffic, traffic_source = measured_traffic("accumulate", wl.name)
     return {
         "metric": "local gradient accumulation, algorithmic GB/s of the accumulate kernel",
         "value": gbps(acc_bytes, t_acc32), "unit": "GB/s", "n_gpus": 1, "steps": reps,
@@ -425,7 +434,8 @@ def bench_accumulate(args, wl):
                     "serial_ms": round(t_serial, 5), "overlapped_ms": round(t_overlap, 5)},
         "roofline": {"bound": "hbm", "kernel": "accumulate", "achieved": gbps(acc_bytes, acc_ms),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(acc_bytes / (acc_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(acc_bytes / (acc_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic, "traffic_source": traffic_source,
                      "avg_launch_us": round(acc_ms * 1e3, 2), "algorithmic_bytes_per_launch": acc_bytes,
                      "finalize_avg_launch_us": round(fin_ms * 1e3, 2),
                      "finalize_GBps": gbps((8.0 + b) * P, fin_ms)},
@@ -514,7 +524,7 @@ def main():
         return
 
     if args.summarize_counters:
-        for f in summarize_counters(args.summarize_counters, args.workload):
+        for f in summarize_counters(args.summarize_counters, args.workload, args.mode):
             print(f)
         return
 

@@ -770,13 +770,18 @@ __global__ __launch_bounds__(kWG) void finalize_i8_kernel(float *__restrict__ ac
     store_i8_lane(codes, scales, n, blk, c, s);
     if (reset) {
         const uint64_t b0 = i8_lane_base(blk);
+        if ((blk + 1) * kI8Block <= n) {
 #pragma unroll
-        for (int q = 0; q < 4; q++)
+            for (int q = 0; q < 4; q++) st_stream((f32x4 *)(acc + I8_ELEM(b0, q, 0)), f32x4{0.0f, 0.0f, 0.0f, 0.0f});
+        } else {
 #pragma unroll
-            for (int r = 0; r < 4; r++) {
-                const uint64_t e = I8_ELEM(b0, q, r);
-                if (e < n) acc[e] = 0.0f;
-            }
+            for (int q = 0; q < 4; q++)
+#pragma unroll
+                for (int r = 0; r < 4; r++) {
+                    const uint64_t e = I8_ELEM(b0, q, r);
+                    if (e < n) acc[e] = 0.0f;
+                }
+        }
     }
 }
 
