@@ -433,8 +433,16 @@ __global__ __launch_bounds__(kWG) void reduce_i8_kernel(const GroupTable gt, uin
     const bool full = e0 + kI8PerLane <= len;
     float *mean = ca.acc_out;  // may alias ca.acc_in (same element, same lane)
     float acc[kI8PerLane];
+    if (ca.acc_in && full) {
 #pragma unroll
-    for (int j = 0; j < kI8PerLane; j++) acc[j] = (ca.acc_in && e0 + j < len) ? ca.acc_in[e0 + j] : 0.0f;
+        for (int q = 0; q < 4; q++) {
+            const f32x4 a = *(const f32x4 *)(ca.acc_in + e0 + 4 * q);
+            acc[4 * q] = a[0]; acc[4 * q + 1] = a[1]; acc[4 * q + 2] = a[2]; acc[4 * q + 3] = a[3];
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < kI8PerLane; j++) acc[j] = (ca.acc_in && e0 + j < len) ? ca.acc_in[e0 + j] : 0.0f;
+    }
     reduce_i8_range<B>(pt, p_lo, p_hi, blk, e0, len, full, acc);
     if (mean) {
         if (full) {
