@@ -7,6 +7,8 @@
 // once, fp32 division and square root are correctly rounded (the HIP
 // defaults), so the results are fixed by the definitions in dedloc.h.
 #include <algorithm>
+#include <tuple>
+#include <utility>
 
 #include "dedloc_internal.h"
 
@@ -804,13 +806,25 @@ static inline unsigned grid_for(uint64_t items, uint64_t per_block) {
     return (unsigned)((items + per_block - 1) / per_block);
 }
 
-#define DEDLOC_LAUNCH(grid, kernel, ...)                                   \
-    do {                                                                   \
-        const dim3 g_ = (grid);                                            \
-        if (g_.x == 0 || g_.y == 0) return hipSuccess; /* nothing to do */ \
-        hipLaunchKernelGGL(kernel, g_, dim3(kWG), 0, __VA_ARGS__);         \
-        return hipGetLastError();                                          \
-    } while (0)
+// Launch through hipLaunchKernel, whose return value is this launch's own
+// status (hipGetLastError after a <<<>>> launch would also report an error
+// left pending by an earlier, unrelated call of the caller's).  The
+// arguments are converted to the kernel's parameter types and held while
+// the runtime copies them into the kernel arguments.
+template <typename K, typename Held, size_t... I>
+static hipError_t launch_held(K kernel, dim3 grid, hipStream_t s, Held &held, std::index_sequence<I...>) {
+    void *argv[] = {(void *)&std::get<I>(held)...};
+    return hipLaunchKernel((const void *)kernel, grid, dim3(kWG), argv, 0, s);
+}
+
+template <typename... KArgs, typename... Args>
+static hipError_t launch_kernel(void (*kernel)(KArgs...), dim3 grid, hipStream_t s, Args &&...args) {
+    if (grid.x == 0 || grid.y == 0) return hipSuccess;  // nothing to do
+    std::tuple<KArgs...> held(std::forward<Args>(args)...);
+    return launch_held(kernel, grid, s, held, std::index_sequence_for<KArgs...>{});
+}
+
+#define DEDLOC_LAUNCH(grid, kernel, s, ...) return launch_kernel((kernel), (grid), (s), __VA_ARGS__)
 
 hipError_t launch_encode_fp16(const float *x, uint64_t n, uint16_t *codes, hipStream_t s) {
     DEDLOC_LAUNCH(dim3(grid_for(n, (uint64_t)kWG * kVec)), encode_fp16_kernel, s, x, n, codes);

@@ -532,3 +532,20 @@ def test_round_full_size_sampled(name):
     assert np.isfinite(trust).all() and (trust > 0).all()
     del dr
     torch.cuda.empty_cache()
+
+
+def test_pending_hip_error_is_not_reported():
+    """A launch reports its own status: an error left pending by an earlier,
+    unrelated HIP call of the caller's (here hipSetDevice on a device that
+    does not exist) does not make a library call fail."""
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so")
+    x = _up(np.linspace(-1, 1, 4096).astype(F))
+    torch.cuda.synchronize()
+    assert hip.hipSetDevice(ctypes.c_int(4096)) != 0  # leaves hipErrorInvalidDevice pending
+    try:
+        codes, _ = D.dedloc_encode(x, D.DEDLOC_CODEC_FP16)
+    finally:
+        hip.hipGetLastError()  # clear it for the rest of the process
+        torch.cuda.set_device(0)
+    assert np.array_equal(_u16(codes), oracle.encode_fp16(_np(x)))
