@@ -164,7 +164,9 @@ int dedloc_reduce_shard(const void *const *peer_codes, const float *const *peer_
 size_t dedloc_lamb_workspace_bytes(uint64_t P, const uint64_t *offsets, uint32_t n_tensors);
 
 /* Zero-fill a device buffer (for example a workspace) with a kernel: no
- * memset node, so the call may be captured into a graph. */
+ * memset node, so the call may be captured into a graph.  ws must be
+ * 4-byte aligned and ws_bytes a multiple of 4 (INVALID_ARG otherwise;
+ * ws_bytes == 0 is a no-op). */
 int dedloc_workspace_clear(void *ws, size_t ws_bytes, void *stream);
 
 /* One LAMB step over a flat parameter buffer (Section 3.1 trains with LAMB;

@@ -591,6 +591,7 @@ size_t dedloc_lamb_workspace_bytes(uint64_t P, const uint64_t *offsets, uint32_t
 
 int dedloc_workspace_clear(void *ws, size_t ws_bytes, void *stream) {
     if (!ws || !aligned(ws, 4)) return fail(DEDLOC_ERR_INVALID_ARG, "workspace must be non-NULL and 4-byte aligned");
+    if (ws_bytes % 4) return fail(DEDLOC_ERR_INVALID_ARG, "ws_bytes must be a multiple of 4 (got %zu)", ws_bytes);
     hipStream_t s = (hipStream_t)stream;
     hipError_t e = timed(K_FILL, s, [&] { return launch_fill_zero(ws, ws_bytes, s); });
     return e == hipSuccess ? DEDLOC_OK : hip_fail(e, "workspace clear launch");

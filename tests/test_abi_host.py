@@ -241,3 +241,12 @@ def test_group_allreduce_validation():
     assert lib.dedloc_group_allreduce_workspace_bytes(1025, 2, 64, D.DEDLOC_CODEC_FP16, 0) == 0
     assert lib.dedloc_group_allreduce_workspace_bytes(8, 65, 64, D.DEDLOC_CODEC_FP16, 0) == 0
     assert lib.dedloc_group_allreduce_workspace_bytes(1024, 32, 64, D.DEDLOC_CODEC_FP16, 0) == 2 * 32 * 256
+
+
+def test_workspace_clear_validation():
+    lib = D.load()
+    A = 1 << 20
+    assert lib.dedloc_workspace_clear(None, 256, None) == D.DEDLOC_ERR_INVALID_ARG
+    assert lib.dedloc_workspace_clear(A + 2, 256, None) == D.DEDLOC_ERR_INVALID_ARG   # alignment
+    assert lib.dedloc_workspace_clear(A, 255, None) == D.DEDLOC_ERR_INVALID_ARG       # not whole words
+    assert lib.dedloc_workspace_clear(A, 0, None) == D.DEDLOC_OK                      # nothing to clear
