@@ -315,6 +315,9 @@ TABLES = {
     "single": [4097],
     "many_small": [64] * 100 + [128] * 30 + [2048 * 3 + 8] * 5 + [19],
     "empty_chunk": [4096] * 64 + [0] * 6,
+    # 450 tensors: three launch chunks of at most 192 tensors, tensor sizes
+    # 0 to 3 tiles, the last one ragged
+    "chunks": [8 * ((i * 37) % 769) for i in range(449)] + [2048 * 3 + 5],
 }
 
 
