@@ -168,6 +168,33 @@ def test_degenerate_round(name, codec, opt):
     _check_round(_degenerate(name, codec, opt))
 
 
+@pytest.mark.parametrize("codec", [FP16, I8])
+@pytest.mark.parametrize("opt", ["lamb", "lars"])
+def test_round_many_chunks(codec, opt):
+    """450 tensors: the optimizer passes run in three launch chunks of at
+    most 192 tensors; with the fp16 codec every chunk's pass A also averages
+    its own range of the messages (and encodes the local peer's)."""
+    print(f"\n[many chunks] codec={codec} opt={opt}", flush=True)
+    rng = np.random.default_rng(4500 + codec)
+    sizes = [8 * int(k) for k in rng.integers(0, 700, 449)] + [2048 * 3 + 5]
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.uint64)
+    P = int(off[-1])
+    n = 6
+    counts = np.array([5, 0, 9, 1, 30, 2], np.uint32)
+    grads = [(rng.standard_normal(P) * 1e-3).astype(F) for _ in range(n)]
+    align = 64 if codec == FP16 else 1024
+    bounds = oracle.partition(P, 4, rng.integers(1, 1000, 4), align)
+    x = (rng.standard_normal(P) * 0.02).astype(F)
+    m = (rng.standard_normal(P) * 1e-4).astype(F)
+    v = np.square(rng.standard_normal(P) * 1e-3).astype(F)
+    if opt == "lamb":
+        cfg = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-6, weight_decay=0.01, step=4)
+    else:
+        cfg = dict(lr=4.8, momentum=0.9, trust_coef=1e-3, weight_decay=1e-5)
+    _check_round(dict(codec=codec, opt=opt, off=off, flags=rng.integers(0, 4, len(sizes)).astype(np.uint8), P=P,
+                      counts=counts, local=2, grads=grads, bounds=bounds, x=x, m=m, v=v, cfg=cfg))
+
+
 def _check_round(c):
     codec, P, counts, local = c["codec"], c["P"], c["counts"], c["local"]
     n = len(counts)
