@@ -112,7 +112,7 @@ def _case(seed):
                 bounds=bounds, x=x, m=m, v=v, cfg=cfg)
 
 
-@pytest.mark.parametrize("seed", range(100))
+@pytest.mark.parametrize("seed", range(300))
 def test_random_round(seed):
     c = _case(seed)
     print(f"\n[seed {seed}] codec={c['codec']} opt={c['opt']} P={c['P']} tensors={len(c['flags'])} "
