@@ -480,7 +480,26 @@ def _superset(a, b, P, codec):
 
 @pytest.mark.parametrize("name", list(W.WORKLOADS))
 def test_round_full_size_sampled(name):
-    wl = W.WORKLOADS[name]
+    _full_size_sampled(W.WORKLOADS[name])
+
+
+# Vectors past 2^31 elements: the largest tensor alone has more than 2^31
+# elements, so element indices, tile numbers, chunk offsets and grid sizes
+# all leave the 32-bit signed range (the stress workload stops at 2^30).
+BEYOND_2P31 = [W.Workload(name=f"beyond_2p31_{c}", cid=20 + i,
+                          tensors=(("big_w", 2 ** 31 + 2 ** 20, "w"), ("mid_w", 2 ** 20, "w"),
+                                   ("tail_g", 2 ** 20 + 13, "g")),
+                          n_peers=3, codec=c, sigma=1e-3, count_range=(1, 64))
+               for i, c in enumerate(("fp16", "i8"))]
+
+
+@pytest.mark.parametrize("wl", BEYOND_2P31, ids=lambda w: w.name)
+def test_round_beyond_2p31_elements(wl):
+    _full_size_sampled(wl)
+
+
+def _full_size_sampled(wl):
+    name = wl.name
     codec = H.codec_id(wl)
     tensors, blocks = _sample(wl)
     off = wl.offsets()
