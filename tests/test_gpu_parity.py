@@ -223,9 +223,9 @@ def test_encode_i8_tiny_blocks():
     tiny = np.float32(2.0 ** -149)
     rng = np.random.default_rng(11)
     blocks = []
-    for amax in [1, 2, 63, 64, 65, 127, 128, 1000, 2 ** 20, 2 ** 23, 2 ** 24]:
-        k = rng.integers(-amax, amax + 1, 1024)
-        k[rng.integers(0, 1024)] = amax
+    for amax in [1, 2, 63, 64, 65, 127, 128, 1000, 2 ** 20, 2 ** 23, 2 ** 24, -150, -190, -300]:
+        k = rng.integers(-abs(amax), abs(amax) + 1, 1024)
+        k[rng.integers(0, 1024)] = amax  # a negative maximum: a / s >= 127.5 saturates at -127
         blocks.append(k.astype(F) * tiny)
     x = np.concatenate(blocks)
     codes, scales = D.dedloc_encode(_up(x), D.DEDLOC_CODEC_I8)

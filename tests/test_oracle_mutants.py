@@ -27,7 +27,14 @@ MUTANTS = [
     ("fp16: subnormal shift off by one", "uint64_t r = shift_rne(sig, -e - 1);", "uint64_t r = shift_rne(sig, -e);"),
     ("fp16: overflow saturates instead of reaching infinity", "if (e > 15) return (uint16_t)(sign | 0x7c00u);",
      "if (e > 15) return (uint16_t)(sign | 0x7bffu);"),
+    ("fp16 decode: subnormal scale", "if (e5 == 0) return s * ldexpf((float)m10, -24);",
+     "if (e5 == 0) return s * ldexpf((float)m10, -25);"),
+    ("fp16 decode: exponent bias", "return s * ldexpf((float)(m10 | 0x400u), (int)e5 - 25);",
+     "return s * ldexpf((float)(m10 | 0x400u), (int)e5 - 24);"),
+    ("fp16: NaN encoded as infinity", "if (e8 == 0xff) return (uint16_t)(sign | (m23 ? 0x7e00u : 0x7c00u));",
+     "if (e8 == 0xff) return (uint16_t)(sign | 0x7c00u);"),
     ("int8: scale over 128", "float s = a / 127.0f;", "float s = a / 128.0f;"),
+    ("int8: negative clamp at -128", "if (q < -127.0f) q = -127.0f;", "if (q < -128.0f) q = -128.0f;"),
     ("int8: truncation instead of rounding", "q = rintf(x[i] / s);", "q = truncf(x[i] / s);"),
     ("int8: clamp at 126", "if (q > 127.0f) q = 127.0f;", "if (q > 126.0f) q = 126.0f;"),
     ("int8 decode: wrong block", "out[i] = (float)codes[i] * scales[i / block];",
@@ -64,6 +71,12 @@ MUTANTS = [
     ("group: a member counted once per group", "ncnt[s] = gt;", "ncnt[s] = cnt[s];"),
     ("accumulate: batch size dropped", "acc[i] = fmaf(b, gi, acc[i]);", "acc[i] = acc[i] + gi;"),
     ("finalize: reciprocal instead of division", "scratch[i] = acc[i] / c;", "scratch[i] = acc[i] * (1.0f / c);"),
+    ("finalize: reset ignored", "    if (reset)\n        for (size_t i = 0; i < n; i++) acc[i] = 0.0f;",
+     "    (void)reset;"),
+    ("accumulate: fp16 codes read as their integer value",
+     "float gi = g_codec == 0 ? ((const float *)g)[i] : f16_to_f32(((const uint16_t *)g)[i]);",
+     "float gi = g_codec == 0 ? ((const float *)g)[i] : (float)((const uint16_t *)g)[i];"),
+    ("group: members weighted by their original counts", "cnt[i] = ncnt[i];", "(void)ncnt;"),
 ]
 
 

@@ -92,6 +92,7 @@ TINY = 2.0 ** -149  # the smallest fp32 subnormal
 @example(np.array([63 * TINY, -TINY, 0.0], np.float32))         # the largest block with s = 0
 @example(np.array([64 * TINY, 3 * TINY, -64 * TINY], np.float32))  # the smallest nonzero scale
 @example(np.array([1e-40, -3e-41, 2e-42], np.float32))          # subnormal scale
+@example(np.array([-150 * TINY, 3 * TINY], np.float32))         # a / s = 150: the clamp at -127 decides
 def test_int8_codec_properties(x):
     codes, scales = oracle.encode_i8(x, 1024)
     dec = oracle.decode_i8(codes, scales, 1024)
