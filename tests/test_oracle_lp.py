@@ -4,7 +4,8 @@ builds:
 
 * compute-bound collaborations reach xi = sum(s)/B (closed form);
 * homogeneous peers that all compute reach the all-reduce rate
-  xi = n*b / (2*(n-1)*P) (Section 3.2's AR-SGD special case, closed form);
+  xi = n*b / (2*(n-1)*P) (Section 3.2's AR-SGD special case, closed form),
+  with b the narrower of download and upload when they differ;
 * with compute to spare, the relaxation reaches its bound xi = 2*b/P: the
   return to oneself g_ii is limited only through (1 - c_k)*d_i, so as c -> 0
   each peer receives d_i from itself plus d_i over the network (closed form
@@ -38,6 +39,17 @@ def test_all_reduce_rate_when_all_compute(n):
     r = lp.solve(s, b, b, B=1.0, P=P, fix_c=np.ones(n))
     assert np.isclose(r["xi"], n * 1e6 / (2 * (n - 1) * P), rtol=1e-6)
     assert np.isclose(r["frac"].sum(), 1.0)
+
+
+@pytest.mark.parametrize("n", [2, 3, 5])
+@pytest.mark.parametrize("down,up", [(1e6, 3e6), (3e6, 1e6)])
+def test_all_reduce_rate_limited_by_the_slower_direction(n, down, up):
+    # every peer sends and returns 2*(n-1)/n of the vector per step in each
+    # direction, so the narrower of download and upload sets the rate
+    s = np.full(n, 1e9)
+    P = 2e6
+    r = lp.solve(s, np.full(n, down), np.full(n, up), B=1.0, P=P, fix_c=np.ones(n))
+    assert np.isclose(r["xi"], n * min(down, up) / (2 * (n - 1) * P), rtol=1e-6)
 
 
 @pytest.mark.parametrize("n", [2, 3, 4, 6])

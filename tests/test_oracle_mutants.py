@@ -80,6 +80,38 @@ MUTANTS = [
 ]
 
 
+# (name, text in oracle/lp.py, replacement): the load-balancing LP, pinned by
+# tests/test_oracle_lp.py
+LP_SRC = os.path.join(ROOT, "oracle", "lp.py")
+LP_MUTANTS = [
+    ("lp: compute rate times B", "[(c(i), -s[i] / B) for i in range(n)]", "[(c(i), -s[i] * B) for i in range(n)]"),
+    ("lp: receive rate from the transposed return rates", "[(g(j, i), -1.0 / P) for j in range(n)]",
+     "[(g(i, j), -1.0 / P) for j in range(n)]"),
+    ("lp: aggregation without the relaxation", "add([(g(i, j), 1.0), (a(k, i), -1.0), (c(k), d[i])], d[i])",
+     "add([(g(i, j), 1.0), (a(k, i), -1.0)], 0.0)"),
+    ("lp: download limited by the upload bandwidth",
+     "add([(a(j, i), 1.0) for j in range(n) if j != i] + [(g(j, i), 1.0) for j in range(n) if j != i], d[i])",
+     "add([(a(j, i), 1.0) for j in range(n) if j != i] + [(g(j, i), 1.0) for j in range(n) if j != i], u[i])"),
+    ("lp: self-traffic charged to the upload",
+     "add([(a(i, j), 1.0) for j in range(n) if j != i] + [(g(i, j), 1.0) for j in range(n) if j != i], u[i])",
+     "add([(a(i, j), 1.0) for j in range(n)] + [(g(i, j), 1.0) for j in range(n)], u[i])"),
+    ("lp: c unbounded above", "[(0, 1)] * n", "[(0, None)] * n"),
+]
+
+
+def _lp_pins_on(src_path):
+    code = ("import sys, importlib.util, oracle\n"
+            f"spec = importlib.util.spec_from_file_location('oracle.lp', {src_path!r})\n"
+            "mod = importlib.util.module_from_spec(spec)\n"
+            "spec.loader.exec_module(mod)\n"
+            "sys.modules['oracle.lp'] = mod\n"
+            "oracle.lp = mod\n"
+            "import pytest\n"
+            "sys.exit(pytest.main(['-x', '-q', '-p', 'no:cacheprovider', 'tests/test_oracle_lp.py']))\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True, timeout=600)
+    return r.returncode
+
+
 def _pins_on(lib_path):
     code = ("import sys, oracle\n"
             f"oracle._LIB = {lib_path!r}\n"
@@ -108,6 +140,23 @@ def test_pins_catch_every_mutant(tmp_path):
         results = list(ex.map(lambda a: _mutant(a[0], *a[1], str(tmp_path)), enumerate(MUTANTS)))
     survivors = [name for name, rc in results if rc == 0]
     assert not survivors, f"mutants the pins do not catch: {survivors}"
+
+
+
+def test_lp_pins_catch_every_mutant(tmp_path):
+    assert _lp_pins_on(LP_SRC) == 0  # the real oracle passes
+    src = open(LP_SRC).read()
+
+    def run(i, name, old, new):
+        assert src.count(old) == 1, f"mutation site not unique or missing: {name}"
+        path = str(tmp_path / f"lp_mutant_{i}.py")
+        open(path, "w").write(src.replace(old, new))
+        return name, _lp_pins_on(path)
+
+    with concurrent.futures.ThreadPoolExecutor(max_workers=4) as ex:
+        results = list(ex.map(lambda a: run(a[0], *a[1]), enumerate(LP_MUTANTS)))
+    survivors = [name for name, rc in results if rc == 0]
+    assert not survivors, f"LP mutants the pins do not catch: {survivors}"
 
 
 if __name__ == "__main__":
