@@ -25,24 +25,31 @@
 namespace {
 
 struct Tableau {
-    int m = 0, ncol = 0;          // rows (constraints), columns (variables + slacks + rhs)
-    std::vector<double> t;        // (m + 1) x ncol, last row = reduced costs, last column = rhs
+    int m = 0, nvar = 0;          // rows (constraints), columns (variables + slacks)
+    std::vector<double> t;        // (m + 1) x nvar row-major; the last row holds the reduced costs
+    std::vector<double> b;        // m + 1 right-hand sides (b[m]: the objective's)
     std::vector<int> basis;       // basic variable of each row
-    double &at(int r, int c) { return t[(size_t)r * ncol + c]; }
+    double &at(int r, int c) { return t[(size_t)r * nvar + c]; }
 };
 
 // Maximise obj . x subject to A x <= b (b >= 0), x >= 0, starting from the
 // slack basis.  Dantzig's entering rule, switching to Bland's rule (smallest
 // index) after a run of degenerate pivots so that the method terminates.
+// The tableau stays sparse: a pivot touches only the rows where the entering
+// column is nonzero, and in them only the pivot row's nonzero columns.
 int simplex(Tableau &T, int max_iter, double eps) {
-    const int m = T.m, rhs = T.ncol - 1;
+    const int m = T.m, nv = T.nvar;
+    std::vector<double> col(m + 1);  // the entering column, gathered
+    std::vector<int> nz;             // nonzero columns of the pivot row
+    nz.reserve(nv);
     int degenerate = 0;
     for (int it = 0; it < max_iter; it++) {
         const bool bland = degenerate > 50;
         int e = -1;
         double best = -eps;
-        for (int j = 0; j < rhs; j++) {
-            const double rc = T.at(m, j);
+        const double *cost = &T.t[(size_t)m * nv];
+        for (int j = 0; j < nv; j++) {
+            const double rc = cost[j];
             if (rc < -eps) {
                 if (bland) {
                     e = j;
@@ -55,12 +62,17 @@ int simplex(Tableau &T, int max_iter, double eps) {
             }
         }
         if (e < 0) return 0;  // optimal
+        const double *ce = &T.t[e];
+        for (int r = 0; r <= m; r++) {
+            if (r + 16 <= m) __builtin_prefetch(ce + (size_t)(r + 16) * nv);
+            col[r] = ce[(size_t)r * nv];
+        }
         int p = -1;
         double ratio = 0.0;
         for (int r = 0; r < m; r++) {
-            const double a = T.at(r, e);
+            const double a = col[r];
             if (a > eps) {
-                const double q = T.at(r, rhs) / a;
+                const double q = T.b[r] / a;
                 if (p < 0 || q < ratio - 1e-15 || (q <= ratio + 1e-15 && T.basis[r] < T.basis[p])) {
                     p = r;
                     ratio = q;
@@ -69,17 +81,23 @@ int simplex(Tableau &T, int max_iter, double eps) {
         }
         if (p < 0) return 1;  // unbounded
         degenerate = ratio <= eps ? degenerate + 1 : 0;
-        const double piv = T.at(p, e);
-        double *prow = &T.t[(size_t)p * T.ncol];
-        for (int c = 0; c < T.ncol; c++) prow[c] /= piv;
+        const double piv = col[p];
+        double *prow = &T.t[(size_t)p * nv];
+        nz.clear();
+        for (int c = 0; c < nv; c++)
+            if (prow[c] != 0.0) {
+                prow[c] /= piv;
+                nz.push_back(c);
+            }
         prow[e] = 1.0;
+        T.b[p] /= piv;
         for (int r = 0; r <= m; r++) {
-            if (r == p) continue;
-            double *row = &T.t[(size_t)r * T.ncol];
-            const double f = row[e];
-            if (f == 0.0) continue;
-            for (int c = 0; c < T.ncol; c++) row[c] -= f * prow[c];
+            const double f = col[r];
+            if (r == p || f == 0.0) continue;
+            double *row = &T.t[(size_t)r * nv];
+            for (const int c : nz) row[c] -= f * prow[c];
             row[e] = 0.0;
+            T.b[r] -= f * T.b[p];
         }
         T.basis[p] = e;
     }
@@ -165,13 +183,14 @@ extern "C" int dedloc_balance(const dedloc_balance_problem *pr, double *xi_out, 
 
     Tableau T;
     T.m = (int)rows.size();
-    T.ncol = nv + T.m + 1;
-    T.t.assign((size_t)(T.m + 1) * T.ncol, 0.0);
+    T.nvar = nv + T.m;
+    T.t.assign((size_t)(T.m + 1) * T.nvar, 0.0);
+    T.b.assign(T.m + 1, 0.0);
     T.basis.resize(T.m);
     for (int r = 0; r < T.m; r++) {
         for (auto &e : rows[r].e) T.at(r, e.first) += e.second;
         T.at(r, nv + r) = 1.0;
-        T.at(r, T.ncol - 1) = rows[r].b;
+        T.b[r] = rows[r].b;
         T.basis[r] = nv + r;
     }
     T.at(T.m, vxi) = -1.0;  // maximise xi
@@ -180,7 +199,7 @@ extern "C" int dedloc_balance(const dedloc_balance_problem *pr, double *xi_out, 
 
     std::vector<double> x(nv, 0.0);
     for (int r = 0; r < T.m; r++)
-        if (T.basis[r] < nv) x[T.basis[r]] = T.at(r, T.ncol - 1);
+        if (T.basis[r] < nv) x[T.basis[r]] = T.b[r];
     *xi_out = x[vxi];
     for (int i = 0; i < n; i++) c_out[i] = x[vc[i]];
     std::vector<double> eff(n, 0.0);
