@@ -167,10 +167,46 @@ def _ptr(t) -> Optional[int]:
     return t.data_ptr()
 
 
-def _dev(t):
-    if t is not None and not t.is_cuda:
-        raise ValueError("expected a device tensor")
-    return _ptr(t)
+def _dev(t, nbytes: Optional[int] = None, name: str = "buffer", f32: bool = False):
+    """Device address of a tensor for the C ABI (None passes as NULL).  The
+    library reads and writes raw memory, so the tensor must be a contiguous
+    device tensor holding at least the `nbytes` the call touches; `f32`:
+    it must also be float32 (a buffer the library reads as fp32)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name}: expected a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: expected a contiguous tensor")
+    if f32 and str(t.dtype) != "torch.float32":
+        raise ValueError(f"{name}: expected float32, got {t.dtype}")
+    if nbytes is not None and t.numel() * t.element_size() < nbytes:
+        raise ValueError(f"{name}: holds {t.numel() * t.element_size()} bytes, the call touches {nbytes}")
+    return t.data_ptr()
+
+
+def _nbytes(t) -> int:
+    return t.numel() * t.element_size()
+
+
+def _code_bytes(codec: int, n: int) -> int:
+    return n * (4 if codec == DEDLOC_CODEC_F32 else 2 if codec == DEDLOC_CODEC_FP16 else 1)
+
+
+def _scale_bytes(codec: int, n: int, block: int) -> int:
+    return 4 * ((n + block - 1) // block) if codec == DEDLOC_CODEC_I8 and block > 0 else 0
+
+
+def _peer_ptrs(ts: Sequence, counts, nbytes: int, name: str) -> ctypes.Array:
+    """Pointer table of the peers' buffers: a peer with samples must hold
+    `nbytes`; a peer without samples is never read (any buffer, or None)."""
+    out = []
+    for p, t in enumerate(ts):
+        if t is None or counts[p] == 0:
+            out.append(None if t is None else t.data_ptr())
+        else:
+            out.append(_dev(t, nbytes, f"{name}[{p}]"))
+    return (ctypes.c_void_p * len(ts))(*out)
 
 
 def _stream(stream=None) -> Optional[int]:
@@ -181,10 +217,6 @@ def _stream(stream=None) -> Optional[int]:
 
 def _host(a, dtype) -> np.ndarray:
     return np.ascontiguousarray(np.asarray(a, dtype=dtype))
-
-
-def _ptrs(ts: Sequence) -> ctypes.Array:
-    return (ctypes.c_void_p * len(ts))(*[None if t is None else _dev(t) for t in ts])
 
 
 # ------------------------------------------------------------- host helpers
@@ -222,7 +254,9 @@ def dedloc_encode(x, codec: int, block: int = DEDLOC_I8_BLOCK, codes=None, scale
         codes = torch.empty(n, dtype=torch.int16 if codec == DEDLOC_CODEC_FP16 else torch.int8, device=x.device)
     if scales is None and codec == DEDLOC_CODEC_I8:
         scales = torch.empty((n + block - 1) // block, dtype=torch.float32, device=x.device)
-    _check(load().dedloc_encode(_dev(x), n, codec, block, _dev(codes), _dev(scales), _stream(stream)))
+    _check(load().dedloc_encode(_dev(x, 4 * n, "x", f32=True), n, codec, block,
+                                _dev(codes, _code_bytes(codec, n), "codes"),
+                                _dev(scales, _scale_bytes(codec, n, block), "scales"), _stream(stream)))
     return codes, scales
 
 
@@ -230,7 +264,9 @@ def dedloc_decode(codes, scales, n: int, codec: int, block: int = DEDLOC_I8_BLOC
     import torch
     if out is None:
         out = torch.empty(n, dtype=torch.float32, device=codes.device)
-    _check(load().dedloc_decode(_dev(codes), _dev(scales), n, codec, block, _dev(out), _stream(stream)))
+    _check(load().dedloc_decode(_dev(codes, _code_bytes(codec, n), "codes"),
+                                _dev(scales, _scale_bytes(codec, n, block), "scales"), n, codec, block,
+                                _dev(out, 4 * n, "out", f32=True), _stream(stream)))
     return out
 
 
@@ -246,10 +282,15 @@ def dedloc_reduce_shard(peer_codes: Sequence, counts, shard_len: int, codec: int
     if out_scales is None and codec == DEDLOC_CODEC_I8:
         out_scales = torch.empty((shard_len + block - 1) // block, dtype=torch.float32, device=dev)
     cnt = _host(counts, np.uint32)
-    pc = _ptrs(peer_codes)
-    ps = None if peer_scales is None else _ptrs(peer_scales)
+    if len(cnt) != len(peer_codes):
+        raise ValueError("counts and peer_codes differ in length")
+    pc = _peer_ptrs(peer_codes, cnt, _code_bytes(codec, shard_len), "peer_codes")
+    ps = None if peer_scales is None else _peer_ptrs(peer_scales, cnt, _scale_bytes(codec, shard_len, block),
+                                                     "peer_scales")
     _check(load().dedloc_reduce_shard(pc, ps, _ptr(cnt), len(peer_codes), shard_len, codec, block,
-                                      _dev(out_codes), _dev(out_scales), _dev(out_mean), _stream(stream)))
+                                      _dev(out_codes, _code_bytes(codec, shard_len), "out_codes"),
+                                      _dev(out_scales, _scale_bytes(codec, shard_len, block), "out_scales"),
+                                      _dev(out_mean, 4 * shard_len, "out_mean", f32=True), _stream(stream)))
     return out_codes, out_scales
 
 
@@ -262,7 +303,7 @@ def dedloc_lamb_workspace_bytes(P: int, offsets) -> int:
 
 
 def dedloc_workspace_clear(ws, stream=None):
-    _check(load().dedloc_workspace_clear(_dev(ws), ws.numel() * ws.element_size(), _stream(stream)))
+    _check(load().dedloc_workspace_clear(_dev(ws, name="ws"), _nbytes(ws), _stream(stream)))
 
 
 def make_workspace(P: int, offsets, device="cuda"):
@@ -281,9 +322,12 @@ def dedloc_lamb_step(x, m, v, grad, offsets, flags, cfg: dedloc_lamb_cfg, grad_c
     P = x.numel()
     if ws is None:
         ws = make_workspace(P, off, x.device)
-    _check(load().dedloc_lamb_step(_dev(x), _dev(m), _dev(v), _dev(grad), _dev(grad_scales), grad_codec, block,
-                                   P, _ptr(off), _ptr(fl), len(fl), ctypes.byref(cfg), _dev(trust_out),
-                                   _dev(ws), ws.numel(), _stream(stream)))
+    _check(load().dedloc_lamb_step(_dev(x, 4 * P, "x", f32=True), _dev(m, 4 * P, "m", f32=True),
+                                   _dev(v, 4 * P, "v", f32=True), _dev(grad, _code_bytes(grad_codec, P), "grad"),
+                                   _dev(grad_scales, _scale_bytes(grad_codec, P, block), "grad_scales"),
+                                   grad_codec, block, P, _ptr(off), _ptr(fl), len(fl), ctypes.byref(cfg),
+                                   _dev(trust_out, 4 * len(fl), "trust_out", f32=True), _dev(ws, name="ws"),
+                                   _nbytes(ws), _stream(stream)))
     return ws
 
 
@@ -294,9 +338,12 @@ def dedloc_lars_step(x, v, grad, offsets, flags, cfg: dedloc_lars_cfg, grad_code
     P = x.numel()
     if ws is None:
         ws = make_workspace(P, off, x.device)
-    _check(load().dedloc_lars_step(_dev(x), _dev(v), _dev(grad), _dev(grad_scales), grad_codec, block, P,
-                                   _ptr(off), _ptr(fl), len(fl), ctypes.byref(cfg), _dev(trust_out),
-                                   _dev(ws), ws.numel(), _stream(stream)))
+    _check(load().dedloc_lars_step(_dev(x, 4 * P, "x", f32=True), _dev(v, 4 * P, "v", f32=True),
+                                   _dev(grad, _code_bytes(grad_codec, P), "grad"),
+                                   _dev(grad_scales, _scale_bytes(grad_codec, P, block), "grad_scales"),
+                                   grad_codec, block, P, _ptr(off), _ptr(fl), len(fl), ctypes.byref(cfg),
+                                   _dev(trust_out, 4 * len(fl), "trust_out", f32=True), _dev(ws, name="ws"),
+                                   _nbytes(ws), _stream(stream)))
     return ws
 
 
@@ -312,10 +359,15 @@ class RoundCall:
         """local: optional (index, fp32 gradient tensor): that peer's message
         buffers are written by the round (dedloc_local_peer)."""
         self._keep = (peer_codes, peer_scales, out_codes, out_scales, x, m, v, ws, trust_out, out_mean, local)
-        self.local = None if local is None else ctypes.byref(dedloc_local_peer(int(local[0]), _dev(local[1])))
-        self.pc = _ptrs(peer_codes)
-        self.ps = None if peer_scales is None else _ptrs(peer_scales)
+        P = x.numel()
+        self.local = None if local is None else ctypes.byref(
+            dedloc_local_peer(int(local[0]), _dev(local[1], 4 * P, "local gradient", f32=True)))
         self.cnt = _host(counts, np.uint32)
+        if len(self.cnt) != len(peer_codes):
+            raise ValueError("counts and peer_codes differ in length")
+        self.pc = _peer_ptrs(peer_codes, self.cnt, _code_bytes(codec, P), "peer_codes")
+        self.ps = None if peer_scales is None else _peer_ptrs(peer_scales, self.cnt, _scale_bytes(codec, P, block),
+                                                              "peer_scales")
         self.bnd = _host(bounds, np.uint64)
         self.off = _host(offsets, np.uint64)
         self.fl = _host(flags, np.uint8)
@@ -323,8 +375,11 @@ class RoundCall:
         self.args = None
         self.codec, self.block = codec, block
         self.lars = isinstance(cfg, dedloc_lars_cfg)
-        self.out = (_dev(out_codes), _dev(out_scales), _dev(x), None if self.lars else _dev(m), _dev(v),
-                    x.numel(), _dev(trust_out), _dev(out_mean), _dev(ws), ws.numel())
+        self.out = (_dev(out_codes, _code_bytes(codec, P), "out_codes"),
+                    _dev(out_scales, _scale_bytes(codec, P, block), "out_scales"), _dev(x, 4 * P, "x", f32=True),
+                    None if self.lars else _dev(m, 4 * P, "m", f32=True), _dev(v, 4 * P, "v", f32=True), P,
+                    _dev(trust_out, 4 * len(self.fl), "trust_out", f32=True),
+                    _dev(out_mean, 4 * P, "out_mean", f32=True), _dev(ws, name="ws"), _nbytes(ws))
 
     def __call__(self, stream=None):
         oc, osc, x, m, v, P, tr, om, ws, wsb = self.out
@@ -432,16 +487,19 @@ class GroupAllreduce:
         self.peer_out = np.zeros(n, dtype=np.uint32)
         self._n_out = ctypes.c_uint32(0)
         self._keep = (peer_codes, peer_scales)
-        self.pc = _ptrs(peer_codes)
-        self.ps = None if peer_scales is None else _ptrs(peer_scales)
         self.cnt = _host(counts, np.uint32)
+        if len(self.cnt) != n:
+            raise ValueError("counts and peer_codes differ in length")
+        self.pc = _peer_ptrs(peer_codes, self.cnt, _code_bytes(codec, length), "peer_codes")
+        self.ps = None if peer_scales is None else _peer_ptrs(peer_scales, self.cnt,
+                                                              _scale_bytes(codec, length, block), "peer_scales")
         self.args = (n, group_size, length, codec, block)
 
     def __call__(self, stream=None):
         n, m, length, codec, block = self.args
         _check(load().dedloc_group_allreduce(self.pc, self.ps, _ptr(self.cnt), n, m, length, codec, block,
                                              _dev(self.out), _dev(self.out_scales), _ptr(self.peer_out),
-                                             ctypes.byref(self._n_out), _dev(self.ws), self.ws.numel(),
+                                             ctypes.byref(self._n_out), _dev(self.ws), _nbytes(self.ws),
                                              _stream(stream)))
         return self
 
@@ -456,7 +514,9 @@ def dedloc_accumulate(acc, grad, batch_samples: float, stream=None):
     """acc += batch_samples * grad (fp32 grad, or fp16 codes as int16)."""
     import torch
     codec = DEDLOC_CODEC_FP16 if grad.dtype in (torch.int16, torch.float16) else DEDLOC_CODEC_F32
-    _check(load().dedloc_accumulate(_dev(acc), _dev(grad), codec, acc.numel(), batch_samples, _stream(stream)))
+    n = acc.numel()
+    _check(load().dedloc_accumulate(_dev(acc, 4 * n, "acc", f32=True), _dev(grad, _code_bytes(codec, n), "grad"),
+                                    codec, n, batch_samples, _stream(stream)))
 
 
 def dedloc_finalize(acc, count: int, codec: int, block: int = DEDLOC_I8_BLOCK, codes=None, scales=None,
@@ -467,7 +527,9 @@ def dedloc_finalize(acc, count: int, codec: int, block: int = DEDLOC_I8_BLOCK, c
         codes = torch.empty(n, dtype=torch.int16 if codec == DEDLOC_CODEC_FP16 else torch.int8, device=acc.device)
     if scales is None and codec == DEDLOC_CODEC_I8:
         scales = torch.empty((n + block - 1) // block, dtype=torch.float32, device=acc.device)
-    _check(load().dedloc_finalize(_dev(acc), n, count, codec, block, _dev(codes), _dev(scales), int(reset),
+    _check(load().dedloc_finalize(_dev(acc, 4 * n, "acc", f32=True), n, count, codec, block,
+                                  _dev(codes, _code_bytes(codec, n), "codes"),
+                                  _dev(scales, _scale_bytes(codec, n, block), "scales"), int(reset),
                                   _stream(stream)))
     return codes, scales
 

@@ -571,3 +571,30 @@ def test_pending_hip_error_is_not_reported():
         hip.hipGetLastError()  # clear it for the rest of the process
         torch.cuda.set_device(0)
     assert np.array_equal(_u16(codes), oracle.encode_fp16(_np(x)))
+
+
+def test_binding_rejects_bad_buffers():
+    """The library reads and writes raw memory, so the Python binding refuses
+    a tensor the call would overrun or misread before anything is launched:
+    non-contiguous or broadcast views, the wrong dtype, too few elements.  A
+    peer without samples is never read, so its buffer is not checked."""
+    n = 4096
+    x = _up(np.linspace(-1, 1, n).astype(F))
+    with pytest.raises(ValueError, match="contiguous"):
+        D.dedloc_encode(torch.zeros(n, 2, device=DEV)[:, 0], D.DEDLOC_CODEC_FP16)
+    with pytest.raises(ValueError, match="contiguous"):
+        D.dedloc_encode(torch.zeros(1, device=DEV).expand(n), D.DEDLOC_CODEC_FP16)
+    with pytest.raises(ValueError, match="float32"):
+        D.dedloc_encode(x.half(), D.DEDLOC_CODEC_FP16)
+    with pytest.raises(ValueError, match="codes"):
+        D.dedloc_encode(x, D.DEDLOC_CODEC_FP16, codes=torch.empty(n - 1, dtype=torch.int16, device=DEV))
+    off, flags = np.array([0, n], np.uint64), np.array([3], np.uint8)
+    with pytest.raises(ValueError, match="m:"):
+        D.dedloc_lamb_step(x.clone(), torch.zeros(n - 8, device=DEV), torch.zeros(n, device=DEV), x, off, flags,
+                           D.lamb_cfg())
+    codes, _ = D.dedloc_encode(x, D.DEDLOC_CODEC_FP16)
+    short = codes[: n // 2]
+    with pytest.raises(ValueError, match=r"peer_codes\[1\]"):
+        D.dedloc_reduce_shard([codes, short], [1, 1], n, D.DEDLOC_CODEC_FP16)
+    out, _ = D.dedloc_reduce_shard([codes, short], [1, 0], n, D.DEDLOC_CODEC_FP16)  # peer 1 is never read
+    assert np.array_equal(_u16(out), _u16(codes))
