@@ -106,7 +106,9 @@ int dedloc_partition(uint64_t P, uint32_t n_shards, const uint64_t *weights,
  * accumulated samples (appendix "Convergence analysis"): peer p, whose mean
  * gradient covers counts[p] samples, gets w[p] = counts[p] / sum(counts),
  * one correctly rounded fp32 division.  sum(counts) must be in [1, 2^24].
- * Errors: all counts zero -> ZERO_WEIGHT; sum above 2^24 -> INVALID_ARG. */
+ * counts and w are host arrays of n entries.
+ * Errors: counts or w NULL, n == 0 -> INVALID_ARG; all counts zero ->
+ * ZERO_WEIGHT; sum above 2^24 -> INVALID_ARG. */
 int dedloc_weights(const uint32_t *counts, uint32_t n, float *w);
 
 /* Encode n fp32 values (the sender's side of the exchange).
@@ -118,11 +120,17 @@ int dedloc_weights(const uint32_t *counts, uint32_t n, float *w);
  *         even; a block with s = 0 (all zero, or max|x| <= 63 * 2^-149 so
  *         that the division underflows) has every q = 0.  codes: int8[n],
  *         scales: float[ceil(n/block)].  Inputs must be finite.
- * n == 0 is a no-op. */
+ * x, codes, scales: device, caller-owned.  n == 0 is a no-op.
+ * Errors: unknown codec or an int8 block other than DEDLOC_I8_BLOCK ->
+ * INVALID_ARG; x or codes NULL (n > 0), or int8 scales NULL -> INVALID_ARG;
+ * x or codes not 16-byte aligned, scales not 4-byte aligned -> ALIGN. */
 int dedloc_encode(const float *x, uint64_t n, int32_t codec, uint32_t block,
                   void *codes, float *scales, void *stream);
 
-/* Decode n elements: fp16 -> fp32 exactly; int8 -> q * s (one rounding). */
+/* Decode n elements: fp16 -> fp32 exactly; int8 -> q * s (one rounding).
+ * codes, scales, out: device, caller-owned, laid out as dedloc_encode
+ * writes them; out is fp32[n].  n == 0 is a no-op.  Errors as for
+ * dedloc_encode (out in place of x). */
 int dedloc_decode(const void *codes, const float *scales, uint64_t n,
                   int32_t codec, uint32_t block, float *out, void *stream);
 
@@ -192,7 +200,14 @@ int dedloc_workspace_clear(void *ws, size_t ws_bytes, void *stream);
  * only when both norms compare greater than 0, so a NaN norm gives r_t = 1;
  * an infinite norm gives 0 or infinity by the division.
  * P = 0 (every tensor empty) is valid: no element is read or written, x,
- * m, v and grad may be NULL, and trust_out receives r = 1 for every tensor. */
+ * m, v and grad may be NULL, and trust_out receives r = 1 for every tensor.
+ * Errors: cfg NULL or step 0 -> INVALID_ARG; offsets NULL, n_tensors 0,
+ * offsets not tiling [0, P), a tensor of 2^32 or more elements, flags NULL
+ * -> INVALID_ARG; an offset (other than P) not a multiple of 8 -> ALIGN;
+ * x, m, v or grad NULL (P > 0) -> INVALID_ARG (grad: ALIGN); a buffer not
+ * 16-byte aligned -> ALIGN; int8 grad without 4-byte aligned grad_scales
+ * -> INVALID_ARG; ws NULL or smaller than dedloc_lamb_workspace_bytes ->
+ * WORKSPACE; ws not 256-byte aligned -> ALIGN. */
 int dedloc_lamb_step(float *x, float *m, float *v, const void *grad,
                      const float *grad_scales, int32_t grad_codec, uint32_t block,
                      uint64_t P, const uint64_t *offsets, const uint8_t *flags,
@@ -248,7 +263,14 @@ typedef struct {
  *               dedloc_reduce_shard);
  *   local       host, nullable: the local peer (dedloc_local_peer).
  * Workspace as dedloc_lamb_workspace_bytes.  P = 0 is valid as for
- * dedloc_lamb_step: the messages, outputs and state may then be NULL. */
+ * dedloc_lamb_step: the messages, outputs and state may then be NULL.
+ * Errors: the peers and counts as for dedloc_reduce_shard; the tensor table,
+ * state, cfg and workspace as for dedloc_lamb_step; bounds NULL, n_shards 0,
+ * bounds not tiling [0, P) -> INVALID_ARG; an int8 interior bound not a
+ * multiple of `block` -> INVALID_ARG; out_codes NULL or misaligned, out_mean
+ * misaligned -> ALIGN; int8 out_scales NULL or misaligned -> INVALID_ARG;
+ * a local peer out of range or without samples -> INVALID_ARG, its
+ * gradient NULL or misaligned -> ALIGN. */
 int dedloc_round(const void *const *peer_codes, const float *const *peer_scales,
                  const uint32_t *counts, uint32_t n_peers, const uint64_t *bounds,
                  uint32_t n_shards, int32_t codec, uint32_t block, void *out_codes,
