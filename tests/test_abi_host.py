@@ -250,3 +250,25 @@ def test_workspace_clear_validation():
     assert lib.dedloc_workspace_clear(A + 2, 256, None) == D.DEDLOC_ERR_INVALID_ARG   # alignment
     assert lib.dedloc_workspace_clear(A, 255, None) == D.DEDLOC_ERR_INVALID_ARG       # not whole words
     assert lib.dedloc_workspace_clear(A, 0, None) == D.DEDLOC_OK                      # nothing to clear
+
+
+def test_codec_and_weights_validation():
+    lib = D.load()
+    A = 1 << 20
+    F, I8 = D.DEDLOC_CODEC_FP16, D.DEDLOC_CODEC_I8
+    assert lib.dedloc_encode(A, 64, 7, 0, A, None, None) == D.DEDLOC_ERR_INVALID_ARG        # codec
+    assert lib.dedloc_encode(A, 64, I8, 512, A, A, None) == D.DEDLOC_ERR_INVALID_ARG       # block
+    assert lib.dedloc_encode(None, 64, F, 0, A, None, None) == D.DEDLOC_ERR_INVALID_ARG
+    assert lib.dedloc_encode(A, 64, I8, 1024, A, None, None) == D.DEDLOC_ERR_INVALID_ARG   # no scales
+    assert lib.dedloc_encode(A + 4, 64, F, 0, A, None, None) == D.DEDLOC_ERR_ALIGN
+    assert lib.dedloc_encode(A, 64, I8, 1024, A, A + 2, None) == D.DEDLOC_ERR_ALIGN
+    assert lib.dedloc_encode(None, 0, F, 0, None, None, None) == D.DEDLOC_OK               # empty
+    assert lib.dedloc_decode(A, None, 64, F, 0, None, None) == D.DEDLOC_ERR_INVALID_ARG
+    assert lib.dedloc_decode(A + 8, None, 64, F, 0, A, None) == D.DEDLOC_ERR_ALIGN
+    assert lib.dedloc_decode(A, None, 64, I8, 1024, A, None) == D.DEDLOC_ERR_INVALID_ARG   # no scales
+    w = np.zeros(2, np.float32)
+    c = np.array([1, 2], np.uint32)
+    assert lib.dedloc_weights(None, 2, w.ctypes.data) == D.DEDLOC_ERR_INVALID_ARG
+    assert lib.dedloc_weights(c.ctypes.data, 0, w.ctypes.data) == D.DEDLOC_ERR_INVALID_ARG
+    big = np.array([1 << 24, 1], np.uint32)
+    assert lib.dedloc_weights(big.ctypes.data, 2, w.ctypes.data) == D.DEDLOC_ERR_INVALID_ARG
