@@ -322,8 +322,9 @@ int dedloc_group_allreduce(const void *const *peer_codes, const float *const *pe
                            float *out_scales, uint32_t *peer_out, uint32_t *n_out, void *ws,
                            size_t ws_bytes, void *stream);
 
-/* Local accumulation (Section 3.1: every peer accumulates gradients at its
- * own pace until the collaboration reaches the target batch).  A micro-batch
+/* Local accumulation (Section 3.1: a peer keeps summing micro-batch
+ * gradients, however fast it runs, until the whole group's sample total
+ * hits the global batch size).  A micro-batch
  * of batch_samples samples whose mean gradient is grad (fp32, or fp16 codes
  * with grad_codec = DEDLOC_CODEC_FP16) is added as
  *     acc[e] = fma(batch_samples, grad[e], acc[e]).

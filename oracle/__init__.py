@@ -9,7 +9,7 @@ Functions and the passages they follow:
   partition  - Section 3.2 / Appendix B (shares proportional to throughput)
   weights    - appendix "Convergence analysis" (mean over all samples)
   encode_*/decode_* - the build's wire codecs (fp16 RNE; int8 absmax/127)
-  reduce     - Section 3.2 (a reducer averages its partition from all senders)
+  reduce     - Section 3.2 (the owner of a share averages every sender's copy of it)
   lamb       - Section 3.1 and the XL appendix (LAMB, layer-wise trust ratio)
   lars       - Section 4.1 (SwAV trains with LARS: layer-wise rate scaling)
   round      - Sections 3.1-3.2 (reduce-scatter, gather, one optimizer step)

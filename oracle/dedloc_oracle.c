@@ -184,8 +184,8 @@ static void encode_any(int codec, const float *x, size_t n, uint32_t block,
 static size_t code_bytes(int codec) { return codec == 1 ? 2 : 1; }
 
 /* ------------------------------------------------------------------------ */
-/* Reducer step (Section 3.2: a receiver accumulates the gradients of its
- * partition from all senders and returns the average).  Peers with zero
+/* Reducer step (Section 3.2: the peer that owns a share of the vector sums
+ * what every sender sent for that share and sends the mean back).  Peers with zero
  * samples have weight 0 and are not read at all (Appendix B: a peer with
  * c_i != 1 disregards its local gradient but still aggregates).
  *     mean[e] = sum over active p, ascending, of w_p * dec_p[e]
@@ -499,8 +499,9 @@ int oracle_group_allreduce(const void *const *peer_codes, const float *const *pe
 }
 
 /* ------------------------------------------------------------------------ */
-/* Local accumulation (Section 3.1: each peer accumulates gradients at its
- * own pace until the collaboration reaches the target batch).  A micro-batch
+/* Local accumulation (Section 3.1: a peer keeps summing micro-batch
+ * gradients, however fast it runs, until the whole group's sample total
+ * hits the global batch size).  A micro-batch
  * of b samples whose mean gradient is g adds b*g to the running sum:
  *     acc = fmaf(b, g, acc)          (one rounding per element per batch)
  * When the round starts the peer's mean gradient is acc / count (one

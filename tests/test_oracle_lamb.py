@@ -3,7 +3,9 @@ used by Section 3.1 and the sahajBERT-XL appendix).
 
 * trust ratio forced to 1 and no weight decay: torch.optim.Adam (float64);
 * trust ratio forced to 1 with decoupled weight decay: torch.optim.AdamW;
-* closed forms at the first step from zero moments (hand-derived fixtures);
+* closed forms at the first step from zero moments (hand-derived fixtures),
+  one with weight decay on one tensor of two, so that the trust ratio's
+  ||u|| includes the decay term and r != 1;
 * an independent float64 numpy statement of the textbook update, within the
   fp32 rounding error;
 * the trust-ratio fallback rules (zero norm, non-adaptive tensor)."""
@@ -61,15 +63,16 @@ def test_golden_closed_forms(golden_dir):
     d = json.load(open(os.path.join(golden_dir, "lamb_examples.json")))
     for c in d["cases"]:
         n = len(c["x"])
+        off = np.array(c.get("offsets", [0, n]), np.uint64)
+        flags = np.array(c.get("flags", [3]), np.uint8)
         cfg = oracle.lamb_cfg(c["lr"], c["beta1"], c["beta2"], c["eps"],
                               c["weight_decay"], step=c["step"])
         x, m, v, trust = oracle.lamb(np.array(c["x"], F), np.array(c["m"], F),
-                                     np.array(c["v"], F), np.array(c["g"], F),
-                                     np.array([0, n], np.uint64), np.array([3], np.uint8), cfg)
+                                     np.array(c["v"], F), np.array(c["g"], F), off, flags, cfg)
         assert np.allclose(x, c["x_new"], rtol=0, atol=c["atol_x"]), c["derivation"]
         assert np.allclose(m, c["m_new"], rtol=c["rtol_moments"], atol=0)
         assert np.allclose(v, c["v_new"], rtol=c["rtol_moments"], atol=0)
-        assert np.isclose(trust[0], c["trust"], rtol=c["rtol_trust"], atol=0)
+        assert np.allclose(trust, np.atleast_1d(c["trust"]), rtol=c["rtol_trust"], atol=0), c["derivation"]
 
 
 def lamb64(x, m, v, g, off, flags, lr, b1, b2, eps, wd, t, unit=False):

@@ -18,7 +18,12 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "dedloc_oracle.c")
 
-# (name, text in the oracle, replacement)
+# pytest -k expression that leaves out the tests built on a float64
+# restatement of the LAMB formula
+NO_FLOAT64 = "not float64"
+
+# (name, text in the oracle, replacement[, -k expression selecting the pins
+# that must catch it])
 MUTANTS = [
     ("partition: share of the wrong peer", "cum += beta ? beta[k - 1] : 1u;", "cum += beta ? beta[k] : 1u;"),
     ("weights: reciprocal instead of division", "w[p] = (float)counts[p] / (float)W;",
@@ -77,6 +82,13 @@ MUTANTS = [
      "float gi = g_codec == 0 ? ((const float *)g)[i] : f16_to_f32(((const uint16_t *)g)[i]);",
      "float gi = g_codec == 0 ? ((const float *)g)[i] : (float)((const uint16_t *)g)[i];"),
     ("group: members weighted by their original counts", "cnt[i] = ncnt[i];", "(void)ncnt;"),
+    # The trust ratio's norms.  These two run with the float64 restatements of
+    # LAMB deselected, so that a pin that does not restate the formula (the
+    # hand-derived closed form with weight decay) has to catch them.
+    ("lamb: decay term left out of ||u||", "su += (double)ue * (double)ue;",
+     "su += (double)(ue - lam * x[e]) * (double)(ue - lam * x[e]);", NO_FLOAT64),
+    ("lamb: ||x - lr*u|| in place of ||x||", "sx += (double)x[e] * (double)x[e];\n            su",
+     "sx += (double)(x[e] - cfg->lr * ue) * (double)(x[e] - cfg->lr * ue);\n            su", NO_FLOAT64),
 ]
 
 
@@ -112,18 +124,19 @@ def _lp_pins_on(src_path):
     return r.returncode
 
 
-def _pins_on(lib_path):
+def _pins_on(lib_path, kexpr=None):
+    k = ['-k', kexpr] if kexpr else []
     code = ("import sys, oracle\n"
             f"oracle._LIB = {lib_path!r}\n"
             "import pytest, glob\n"
             "files = sorted(glob.glob('tests/test_oracle_*.py'))\n"
             f"files = [f for f in files if not f.endswith({os.path.basename(__file__)!r})]\n"
-            "sys.exit(pytest.main(['-x', '-q', '-p', 'no:cacheprovider', '-m', 'not gpu'] + files))\n")
+            f"sys.exit(pytest.main(['-x', '-q', '-p', 'no:cacheprovider', '-m', 'not gpu'] + {k!r} + files))\n")
     r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True, timeout=600)
     return r.returncode
 
 
-def _mutant(i, name, old, new, tmp):
+def _mutant(i, name, old, new, tmp, kexpr=None):
     src = open(SRC).read()
     assert src.count(old) == 1, f"mutation site not unique or missing: {name}"
     c = os.path.join(tmp, f"mutant_{i}.c")
@@ -131,13 +144,14 @@ def _mutant(i, name, old, new, tmp):
     open(c, "w").write(src.replace(old, new))
     subprocess.check_call(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off", "-fno-fast-math",
                            c, "-o", lib, "-lm"])
-    return name, _pins_on(lib)
+    return name, _pins_on(lib, kexpr)
 
 
 def test_pins_catch_every_mutant(tmp_path):
     assert _pins_on(os.path.join(ROOT, "oracle", "liboracle.so")) == 0  # the real oracle passes
+    assert _pins_on(os.path.join(ROOT, "oracle", "liboracle.so"), NO_FLOAT64) == 0
     with concurrent.futures.ThreadPoolExecutor(max_workers=4) as ex:
-        results = list(ex.map(lambda a: _mutant(a[0], *a[1], str(tmp_path)), enumerate(MUTANTS)))
+        results = list(ex.map(lambda a: _mutant(a[0], *a[1][:3], str(tmp_path), *a[1][3:]), enumerate(MUTANTS)))
     survivors = [name for name, rc in results if rc == 0]
     assert not survivors, f"mutants the pins do not catch: {survivors}"
 

@@ -1,5 +1,5 @@
-"""Pins for the oracle's reducer (Section 3.2: a receiver averages its
-partition from all senders; weighting by accumulated samples per the
+"""Pins for the oracle's reducer (Section 3.2: the owner of a share
+averages every sender's copy of it; weighting by accumulated samples per the
 appendix 'Convergence analysis').
 
 * hand-derived dyadic fixtures (exact);
