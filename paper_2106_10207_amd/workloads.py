@@ -31,8 +31,9 @@ FLAG_DECAY = 1
 FLAG_ADAPT = 2
 
 # kinds: 'w' weight matrix / conv kernel, 'g' normalisation gain, 'b' bias or
-# normalisation shift.
-_KIND_FLAGS = {"w": FLAG_DECAY | FLAG_ADAPT, "g": FLAG_ADAPT, "b": FLAG_ADAPT}
+# normalisation shift, 'd' a tensor with weight decay but no trust ratio
+# (its update is elementwise: r = 1).
+_KIND_FLAGS = {"w": FLAG_DECAY | FLAG_ADAPT, "g": FLAG_ADAPT, "b": FLAG_ADAPT, "d": FLAG_DECAY}
 
 
 @dataclasses.dataclass(frozen=True)
