@@ -279,6 +279,31 @@ int dedloc_round(const void *const *peer_codes, const float *const *peer_scales,
                  const dedloc_lamb_cfg *cfg, float *trust_out, float *out_mean,
                  const dedloc_local_peer *local, void *ws, size_t ws_bytes, void *stream);
 
+/* For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The same
+ * round as dedloc_round (same arguments, kernels, results and errors) but
+ * without the workspace argument: the LAMB workspace is a static device
+ * array of DEDLOC_NOALLOC_SCRATCH_BYTES held by every GPU the library runs
+ * on until the process ends.  The call allocates no device memory.
+ *   - the round's workspace (dedloc_lamb_workspace_bytes of the tensor table,
+ *     about 16 bytes per 2048 elements) must fit the array: at most about
+ *     2^31 elements; larger tables -> DEDLOC_ERR_WORKSPACE before anything
+ *     is launched (use dedloc_round with a workspace of its own);
+ *   - `stream` must belong to the current device (INVALID_ARG otherwise);
+ *     the array's address on that device is looked up at the first call
+ *     there (a failed lookup -> DEDLOC_ERR_HIP);
+ *   - every call on one GPU shares that GPU's array, and the array needs no
+ *     initialisation: calls that overlap in time on one GPU (two streams,
+ *     two threads) race on it and must not be issued. */
+#define DEDLOC_NOALLOC_SCRATCH_BYTES (16u << 20)
+int dedloc_round_noalloc(const void *const *peer_codes, const float *const *peer_scales,
+                         const uint32_t *counts, uint32_t n_peers, const uint64_t *bounds,
+                         uint32_t n_shards, int32_t codec, uint32_t block, void *out_codes,
+                         float *out_scales, float *x, float *m, float *v, uint64_t P,
+                         const uint64_t *offsets, const uint8_t *flags, uint32_t n_tensors,
+                         const dedloc_lamb_cfg *cfg, float *trust_out, float *out_mean,
+                         const dedloc_local_peer *local, void *stream);
+
 /* The same round with the LARS step (dedloc_lars_step) in place of LAMB;
  * v is the momentum buffer.  The fp16 path reads each peer byte once; pass B
  * reads the gathered message, x and v again. */

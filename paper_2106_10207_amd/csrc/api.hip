@@ -17,6 +17,11 @@
 
 using namespace dedloc;
 
+// The workspace of dedloc_round_noalloc.  In host code `scratch` names a
+// host-side stand-in, not device memory: its device address (one per GPU)
+// comes from hipGetSymbolAddress and only that address is handed to kernels.
+static __device__ __align__(256) unsigned char scratch[DEDLOC_NOALLOC_SCRATCH_BYTES];
+
 namespace {
 
 thread_local std::string g_err;
@@ -315,11 +320,17 @@ int lars_params(const dedloc_lars_cfg *cfg, OptParams &op) {
 // x and the optimizer state (m and v for LAMB, the momentum v for LARS).
 // An empty vector (P == 0) reads and writes no element: its buffers may be
 // NULL; only the workspace (the per-tensor ratios) is used.
-int check_state(int opt, float *x, float *m, float *v, uint64_t P, void *ws, size_t ws_bytes, const Plan &pl) {
+// ws == kNoWs: the caller brings no workspace (the static array is used;
+// its size is checked by the caller of this function).
+void *const kNoWs = nullptr;
+
+int check_state(int opt, float *x, float *m, float *v, uint64_t P, void *ws, size_t ws_bytes, const Plan &pl,
+                bool check_ws = true) {
     if (P > 0 && (!x || !v || (opt == kOptLamb && !m)))
         return fail(DEDLOC_ERR_INVALID_ARG, "parameter and state buffers must not be NULL");
     if (!aligned(x, 16) || !aligned(v, 16) || (m && !aligned(m, 16)))
         return fail(DEDLOC_ERR_ALIGN, "parameter and state buffers must be 16-byte aligned");
+    if (!check_ws) return DEDLOC_OK;
     if (!ws || ws_bytes < pl.ws_total)
         return fail(DEDLOC_ERR_WORKSPACE, "workspace of %zu bytes needed (got %zu)", pl.ws_total,
                     ws ? ws_bytes : (size_t)0);
@@ -378,7 +389,7 @@ int prepare_round(int opt, const void *const *peer_codes, const float *const *pe
                   int32_t codec, uint32_t block, void *out_codes, float *out_scales, float *x, float *m,
                   float *v, uint64_t P, const uint64_t *offsets, const uint8_t *flags, uint32_t n_tensors,
                   float *out_mean, const dedloc_local_peer *local, void *ws, size_t ws_bytes,
-                  PeerList &peers, Plan &pl, LocalArgs &la) {
+                  PeerList &peers, Plan &pl, LocalArgs &la, bool check_ws = true) {
     int rc = check_codec(codec, block, false);
     if (rc) return rc;
     rc = build_peers(peer_codes, peer_scales, counts, n_peers, codec, peers, P > 0);
@@ -406,7 +417,7 @@ int prepare_round(int opt, const void *const *peer_codes, const float *const *pe
     if (rc) return rc;
     if (!flags) return fail(DEDLOC_ERR_INVALID_ARG, "flags must not be NULL");
     make_plan(P, offsets, flags, n_tensors, pl);
-    rc = check_state(opt, x, m, v, P, ws, ws_bytes, pl);
+    rc = check_state(opt, x, m, v, P, ws, ws_bytes, pl, check_ws);
     if (rc) return rc;
     if (P == 0) return DEDLOC_OK;
     if (!out_codes || !aligned(out_codes, 16)) return fail(DEDLOC_ERR_ALIGN, "out_codes must be non-NULL and 16-byte aligned");
@@ -449,6 +460,34 @@ int run_round(int opt, const PeerList &peers, int32_t codec, void *out_codes, fl
     int rc = run_reduce(codec, peers, 0, peers.n(), true, P, out_codes, out_scales, out_mean, none, s);
     if (rc) return rc;
     return run_opt(opt, kSrcI8, kSrcI8, pl, nullptr, gathered, gathered, op, x, m, v, ws, trust_out, s);
+}
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];  // device address of `scratch` per device (null: not looked up yet)
+
+// The address of this GPU's static scratch array: the current device, which
+// `stream` must belong to.  Looked up once per device.
+int noalloc_scratch(hipStream_t stream, void **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(DEDLOC_ERR_INVALID_ARG, "device %d is beyond %d", dev, kMaxDevices);
+    hipDevice_t sdev = -1;
+    e = hipStreamGetDevice(stream, &sdev);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamGetDevice");
+    if (sdev != dev)
+        return fail(DEDLOC_ERR_INVALID_ARG, "the stream belongs to device %d, the current device is %d", (int)sdev, dev);
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        if (!p || !aligned(p, 256)) return fail(DEDLOC_ERR_HIP, "the static scratch array has no usable address");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return DEDLOC_OK;
 }
 
 // Group all-reduce layout: m^d slots, m^(d-1) groups per iteration, every
@@ -644,6 +683,33 @@ int dedloc_round(const void *const *peer_codes, const float *const *peer_scales,
     rc = prepare_round(kOptLamb, peer_codes, peer_scales, counts, n_peers, bounds, n_shards, codec, block,
                        out_codes, out_scales, x, m, v, P, offsets, flags, n_tensors, out_mean, local, ws, ws_bytes,
                        peers, pl, la);
+    if (rc) return rc;
+    return run_round(kOptLamb, peers, codec, out_codes, out_scales, x, m, v, P, pl, op, trust_out, out_mean, la,
+                     ws, (hipStream_t)stream);
+}
+
+int dedloc_round_noalloc(const void *const *peer_codes, const float *const *peer_scales, const uint32_t *counts,
+                         uint32_t n_peers, const uint64_t *bounds, uint32_t n_shards, int32_t codec, uint32_t block,
+                         void *out_codes, float *out_scales, float *x, float *m, float *v, uint64_t P,
+                         const uint64_t *offsets, const uint8_t *flags, uint32_t n_tensors,
+                         const dedloc_lamb_cfg *cfg, float *trust_out, float *out_mean,
+                         const dedloc_local_peer *local, void *stream) {
+    OptParams op;
+    int rc = lamb_params(cfg, op);
+    if (rc) return rc;
+    PeerList peers;
+    Plan pl;
+    LocalArgs la;
+    rc = prepare_round(kOptLamb, peer_codes, peer_scales, counts, n_peers, bounds, n_shards, codec, block,
+                       out_codes, out_scales, x, m, v, P, offsets, flags, n_tensors, out_mean, local, kNoWs, 0,
+                       peers, pl, la, /*check_ws=*/false);
+    if (rc) return rc;
+    if (pl.ws_total > DEDLOC_NOALLOC_SCRATCH_BYTES)
+        return fail(DEDLOC_ERR_WORKSPACE,
+                    "this tensor table needs %zu bytes of workspace, more than the %u of the static scratch array "
+                    "(call dedloc_round with a workspace)", pl.ws_total, (unsigned)DEDLOC_NOALLOC_SCRATCH_BYTES);
+    void *ws = nullptr;
+    rc = noalloc_scratch((hipStream_t)stream, &ws);
     if (rc) return rc;
     return run_round(kOptLamb, peers, codec, out_codes, out_scales, x, m, v, P, pl, op, trust_out, out_mean, la,
                      ws, (hipStream_t)stream);

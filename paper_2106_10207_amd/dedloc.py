@@ -29,6 +29,7 @@ DEDLOC_CODEC_F32 = 0
 DEDLOC_CODEC_FP16 = 1
 DEDLOC_CODEC_I8 = 2
 DEDLOC_I8_BLOCK = 1024
+DEDLOC_NOALLOC_SCRATCH_BYTES = 16 << 20  # static workspace of dedloc_round_noalloc
 DEDLOC_MAX_PEERS = 1024
 DEDLOC_MAX_GROUP_PEERS = 1024
 DEDLOC_MAX_GROUP_SIZE = 64
@@ -107,6 +108,11 @@ _SIGS = {
                       ctypes.c_void_p, ctypes.c_uint32, ctypes.POINTER(dedloc_lamb_cfg), ctypes.c_void_p,
                       ctypes.c_void_p, ctypes.POINTER(dedloc_local_peer), ctypes.c_void_p, ctypes.c_size_t,
                       ctypes.c_void_p], ctypes.c_int),
+    "dedloc_round_noalloc": ([ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32, ctypes.c_void_p,
+                              ctypes.c_uint32, ctypes.c_int32, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p,
+                              ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p,
+                              ctypes.c_void_p, ctypes.c_uint32, ctypes.POINTER(dedloc_lamb_cfg), ctypes.c_void_p,
+                              ctypes.c_void_p, ctypes.POINTER(dedloc_local_peer), ctypes.c_void_p], ctypes.c_int),
     "dedloc_lars_step": ([ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                           ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint32,
                           ctypes.POINTER(dedloc_lars_cfg), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
@@ -357,7 +363,9 @@ class RoundCall:
                  cfg, ws, peer_scales=None, out_scales=None, trust_out=None,
                  out_mean=None, block: int = DEDLOC_I8_BLOCK, local=None):
         """local: optional (index, fp32 gradient tensor): that peer's message
-        buffers are written by the round (dedloc_local_peer)."""
+        buffers are written by the round (dedloc_local_peer).  ws None with a
+        LAMB cfg: the call is dedloc_round_noalloc (the library's static
+        workspace)."""
         self._keep = (peer_codes, peer_scales, out_codes, out_scales, x, m, v, ws, trust_out, out_mean, local)
         P = x.numel()
         self.local = None if local is None else ctypes.byref(
@@ -379,7 +387,8 @@ class RoundCall:
                     _dev(out_scales, _scale_bytes(codec, P, block), "out_scales"), _dev(x, 4 * P, "x", f32=True),
                     None if self.lars else _dev(m, 4 * P, "m", f32=True), _dev(v, 4 * P, "v", f32=True), P,
                     _dev(trust_out, 4 * len(self.fl), "trust_out", f32=True),
-                    _dev(out_mean, 4 * P, "out_mean", f32=True), _dev(ws, name="ws"), _nbytes(ws))
+                    _dev(out_mean, 4 * P, "out_mean", f32=True), _dev(ws, name="ws"),
+                    0 if ws is None else _nbytes(ws))
 
     def __call__(self, stream=None):
         oc, osc, x, m, v, P, tr, om, ws, wsb = self.out
@@ -389,6 +398,11 @@ class RoundCall:
                                        len(self.bnd) - 1, self.codec, self.block, oc, osc, x, v, P,
                                        _ptr(self.off), _ptr(self.fl), len(self.fl), ctypes.byref(self.cfg),
                                        tr, om, self.local, ws, wsb, _stream(stream))
+        elif ws is None:
+            rc = lib.dedloc_round_noalloc(self.pc, self.ps, _ptr(self.cnt), len(self.cnt), _ptr(self.bnd),
+                                          len(self.bnd) - 1, self.codec, self.block, oc, osc, x, m, v, P,
+                                          _ptr(self.off), _ptr(self.fl), len(self.fl), ctypes.byref(self.cfg),
+                                          tr, om, self.local, _stream(stream))
         else:
             rc = lib.dedloc_round(self.pc, self.ps, _ptr(self.cnt), len(self.cnt), _ptr(self.bnd),
                                   len(self.bnd) - 1, self.codec, self.block, oc, osc, x, m, v, P,
@@ -412,6 +426,18 @@ def dedloc_round(peer_codes, counts, bounds, codec: int, x, m, v, offsets, flags
     if ws is None:
         ws = make_workspace(P, offsets, x.device)
     RoundCall(peer_codes, counts, bounds, codec, out_codes, x, m, v, offsets, flags, cfg, ws, peer_scales,
+              out_scales, trust_out, out_mean, block, local)(stream)
+    return out_codes, out_scales
+
+
+def dedloc_round_noalloc(peer_codes, counts, bounds, codec: int, x, m, v, offsets, flags,
+                         cfg: dedloc_lamb_cfg, out_codes, out_scales=None, peer_scales=None,
+                         block: int = DEDLOC_I8_BLOCK, trust_out=None, out_mean=None, stream=None, local=None):
+    """dedloc_round without a workspace (the library's static array) and
+    with caller-provided outputs: nothing is allocated."""
+    if isinstance(cfg, dedloc_lars_cfg):
+        raise ValueError("dedloc_round_noalloc takes a LAMB cfg")
+    RoundCall(peer_codes, counts, bounds, codec, out_codes, x, m, v, offsets, flags, cfg, None, peer_scales,
               out_scales, trust_out, out_mean, block, local)(stream)
     return out_codes, out_scales
 

@@ -190,6 +190,34 @@ def test_round_validation_before_launch():
     cnt[1] = 1
 
 
+def test_round_noalloc_validation_before_launch():
+    """The no-allocation round validates like dedloc_round and refuses a
+    tensor table whose workspace exceeds its static array, before it looks
+    the array up on the device or launches anything (no GPU here)."""
+    lib = D.load()
+    A = 1 << 20
+    cfg = D.lamb_cfg(step=1)
+    pc = (ctypes.c_void_p * 2)(A, A)
+    cnt = np.array([1, 1], np.uint32)
+
+    def call(P, off, bounds=None):
+        off = np.asarray(off, np.uint64)
+        fl = np.full(len(off) - 1, 3, np.uint8)
+        b = np.asarray([0, P] if bounds is None else bounds, np.uint64)
+        return lib.dedloc_round_noalloc(pc, None, cnt.ctypes.data, 2, b.ctypes.data, len(b) - 1,
+                                        D.DEDLOC_CODEC_FP16, 0, A, None, A, A, A, P, off.ctypes.data,
+                                        fl.ctypes.data, len(fl), ctypes.byref(cfg), None, None, None, None)
+    assert call(4096, [0, 2048, 4096], [0, 100, 4095]) == D.DEDLOC_ERR_INVALID_ARG
+    assert call(4096, [0, 2047, 4096]) == D.DEDLOC_ERR_ALIGN
+    # 2^31 + 2^30 elements in two tensors: 3 * 2^20 tiles, 48 MiB of partials
+    big = 3 << 30
+    assert _ws_expected([big // 2, big // 2]) > D.DEDLOC_NOALLOC_SCRATCH_BYTES
+    assert call(big, [0, big // 2, big]) == D.DEDLOC_ERR_WORKSPACE
+    assert "static scratch" in lib.dedloc_last_error().decode()
+    # the largest vector it takes: partials of 2^20 tiles and the ratios
+    assert _ws_expected([(1 << 31) - 2048 * 256]) <= D.DEDLOC_NOALLOC_SCRATCH_BYTES
+
+
 def _ws_expected(sizes, tile=2048):
     tiles = sum((n + tile - 1) // tile for n in sizes)
     r = lambda v: (v + 255) // 256 * 256
