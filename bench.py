@@ -54,6 +54,9 @@ def _parse():
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES, 10 times "
                          "(calibrates HBM byte counters), then exit")
+    ap.add_argument("--summarize-trace", metavar="DIR", default=None,
+                    help="only turn the rocprofv3 --kernel-trace --stats run under DIR "
+                         "(run_kernel_stats.csv) into profiles/kernel_stats_<workload>.json, then exit")
     ap.add_argument("--summarize-counters", metavar="DIR", default=None,
                     help="only turn the rocprofv3 counter runs under DIR (pmc_FETCH_SIZE, "
                          "pmc_WRITE_SIZE, pmc_copy_FETCH_SIZE, pmc_copy_WRITE_SIZE) into "
@@ -142,6 +145,8 @@ def summarize_counters(root_dir, workload, mode="round"):
             "copy_calibration": {"bytes": copy_bytes, "fetch_scale": scale["FETCH_SIZE"],
                                  "write_scale": scale["WRITE_SIZE"]},
             "hbm_bytes_per_launch": fb + wb, "read_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+            "bytes_kind": "L2 <-> fabric (FETCH_SIZE / WRITE_SIZE count L2 misses and write-backs; "
+                          "Infinity Cache hits are included, so these are not DRAM bytes)",
             "commands": [c.format(c=k, w=workload, m=mode) for c in COUNTER_COMMANDS
                          for k in ("FETCH_SIZE", "WRITE_SIZE")],
             "kernels_hip_sha256": digest,
@@ -150,6 +155,65 @@ def summarize_counters(root_dir, workload, mode="round"):
         json.dump(rec, open(out, "w"), indent=1)
         written.append(out)
     return written
+
+
+TRACE_COMMAND = ("rocprofv3 --kernel-trace --stats --output-format csv -d DIR -o run -- "
+                 "python3 bench.py --workload {w} {extra}--no-cpu-baseline")
+
+
+def _kernel_source_digest():
+    import hashlib
+    root = os.path.dirname(os.path.abspath(__file__))
+    return hashlib.sha256(open(os.path.join(root, "paper_2106_10207_amd", "csrc", "kernels.hip"),
+                               "rb").read()).hexdigest()
+
+
+def summarize_trace(root_dir, workload, extra=""):
+    """Average, minimum and maximum duration and call count of every library
+    kernel instance from a rocprofv3 --kernel-trace --stats run, with the
+    hash of the kernel source it was taken with."""
+    import csv
+    rows = {}
+    for r in csv.DictReader(open(os.path.join(root_dir, "run_kernel_stats.csv"))):
+        name = r["Name"].split("(")[0]
+        if "dedloc::" not in name:
+            continue
+        rows[name] = {"calls": int(r["Calls"]), "avg_us": float(r["AverageNs"]) / 1e3,
+                      "min_us": float(r["MinNs"]) / 1e3, "max_us": float(r["MaxNs"]) / 1e3,
+                      "kind": KERNEL_KINDS.get(name)}
+    root = os.path.dirname(os.path.abspath(__file__))
+    rec = {"workload": workload, "command": TRACE_COMMAND.format(w=workload, extra=extra),
+           "kernels": rows, "kernels_hip_sha256": _kernel_source_digest()}
+    out = os.path.join(root, "profiles", f"kernel_stats_{workload}.json")
+    json.dump(rec, open(out, "w"), indent=1)
+    return out
+
+
+def _instance(kind, dr):
+    """rocprofv3's name of the kernel instance a step of `dr` launches for `kind`."""
+    src = 5 if dr.local_in_kernel else (4 if int(np.count_nonzero(dr.counts)) > 64 else 3)
+    names = {"lamb_a_fused_fp16": f"void dedloc::opt_a_kernel<{src}, 0>",
+             "lars_a_fused_fp16": f"void dedloc::opt_a_kernel<{src}, 1>",
+             "reduce_i8": "void dedloc::reduce_i8_kernel<16>",
+             "lamb_b": "void dedloc::opt_b_kernel<0, 0>",
+             "lamb_a_i8": "void dedloc::opt_a_kernel<2, 0>"}
+    return names.get(kind)
+
+
+def rocprof_average_us(kind, dr):
+    """The committed rocprofv3 average duration of the step's `kind` kernel
+    for this workload, or (None, why) when there is none or the kernel
+    source changed since."""
+    root = os.path.dirname(os.path.abspath(__file__))
+    path = os.path.join(root, "profiles", f"kernel_stats_{dr.wl.name}.json")
+    if not os.path.exists(path):
+        return None, None
+    rec = json.load(open(path))
+    rel = os.path.relpath(path, root)
+    if rec.get("kernels_hip_sha256") != _kernel_source_digest():
+        return None, rel + " (stale: kernel source changed)"
+    k = rec["kernels"].get(_instance(kind, dr))
+    return (k["avg_us"], rel) if k else (None, rel)
 
 
 def kernel_roofline(dr, prof, steps):
@@ -194,7 +258,7 @@ def kernel_roofline(dr, prof, steps):
     # chunked kernels launch several times per step; bytes per launch scale
     nbytes = per_launch.get(name, 0.0) / per_step
     achieved = nbytes / (avg_ms * 1e-3) / 1e9
-    return name, {
+    roof = {
         "bound": "hbm",
         "kernel": name,
         "achieved": round(achieved, 1),
@@ -204,7 +268,18 @@ def kernel_roofline(dr, prof, steps):
         "traffic": None,
         "avg_launch_us": round(avg_ms * 1e3, 2),
         "algorithmic_bytes_per_launch": nbytes,
-    }, {k: _kernel_entry(v, steps, per_launch.get(k)) for k, v in prof.items()}
+    }
+    if name.endswith("_fused_fp16") and loc:
+        # the local peer's 4P gradient read is its encode's (a sender-side
+        # step), not the round's: the pass's share of the round's own bytes
+        strict = nbytes - loc * P / per_step
+        roof["round_bytes_per_launch"] = strict
+        roof["frac_round_bytes"] = round(strict / (avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)
+    rp_us, rp_src = rocprof_average_us(name, dr)
+    roof["rocprof_avg_launch_us"] = None if rp_us is None else round(rp_us, 2)
+    roof["frac_rocprof"] = None if rp_us is None else round(nbytes / (rp_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
+    roof["rocprof_source"] = rp_src
+    return name, roof, {k: _kernel_entry(v, steps, per_launch.get(k)) for k, v in prof.items()}
 
 
 def _kernel_entry(v, steps, step_bytes):
@@ -443,12 +518,15 @@ def bench_accumulate(args, wl):
 
 
 def cpu_baseline(wl, dr, reps):
-    """The oracle (plain sequential C) on the same workload: one local encode
-    plus one round, on the host, timed after its inputs are prepared."""
-    import torch
+    """The oracle (plain C, no contraction) on the same workload: one local
+    encode plus one round, on the host, timed after its inputs are prepared.
+    Built for this host's CPU (-O3 -march=native) with its element loops
+    split statically over OpenMP threads; timed on one thread and on every
+    thread this process may use, and the two runs' outputs are compared bit
+    for bit."""
     import oracle
     from paper_2106_10207_amd import workloads as W
-    oracle.build(force=False)
+    oracle.use_library(oracle.build_fast())
     codec = 1 if wl.codec == "fp16" else 2
     codes, scales = [], []
     local_grad = None
@@ -463,49 +541,77 @@ def cpu_baseline(wl, dr, reps):
         if p == dr.local:
             local_grad = g
         del g
-    x, m, v = (t.cpu().numpy() for t in W.optimizer_state(wl, "cuda"))
+    state = [t.cpu().numpy() for t in W.optimizer_state(wl, "cuda")]
     if dr.optimizer == "lamb":
         cfg = oracle.lamb_cfg(wl.lr, wl.beta1, wl.beta2, wl.eps, wl.weight_decay, step=wl.step)
     else:
         cfg = oracle.lars_cfg(wl.lars_lr, wl.lars_momentum, wl.lars_trust_coef, wl.lars_weight_decay)
     bw = W.bandwidth_weights(wl)
-    times = []
-    for _ in range(reps):
-        t0 = time.perf_counter()
+
+    def step():
+        x, m, v = state  # the oracle's round copies its state arguments
         bounds = oracle.partition(wl.P, wl.n_shards, bw, wl.shard_align)
         if codec == 1:
             oracle.encode_fp16(local_grad)
         else:
             oracle.encode_i8(local_grad, 1024)
         if dr.optimizer == "lamb":
-            oracle.round_(codes, dr.counts, bounds, codec, x, m, v, wl.offsets(), wl.flags(), cfg,
-                          scales or None, 1024)
-        else:
-            oracle.round_lars(codes, dr.counts, bounds, codec, x, m, wl.offsets(), wl.flags(), cfg,
-                              scales or None, 1024)
-        times.append(time.perf_counter() - t0)
-    t = float(np.median(times))
+            return oracle.round_(codes, dr.counts, bounds, codec, x, m, v, wl.offsets(), wl.flags(), cfg,
+                                 scales or None, 1024)
+        return oracle.round_lars(codes, dr.counts, bounds, codec, x, m, wl.offsets(), wl.flags(), cfg,
+                                 scales or None, 1024)
+
+    def timed(threads, n):
+        oracle.threads(threads)
+        times, out = [], None
+        for _ in range(n):
+            t0 = time.perf_counter()
+            out = step()
+            times.append(time.perf_counter() - t0)
+        return float(np.median(times)), out
+
+    all_threads = int(os.environ.get("OMP_NUM_THREADS") or 0) or len(os.sched_getaffinity(0))
+    all_threads = min(all_threads, len(os.sched_getaffinity(0)))
+    t1, r1 = timed(1, max(1, min(reps, 3)))
+    tn, rn = timed(all_threads, reps)
+    same = all(np.array_equal(np.asarray(r1[k]).view(np.uint8), np.asarray(rn[k]).view(np.uint8))
+               for k in r1 if r1[k] is not None)
+    peer = dr.bytes_peer_input()
     return {
-        "value": round(dr.bytes_peer_input() / t / 1e9, 4),
+        "value": round(peer / tn / 1e9, 4),
         "unit": "GB/s",
-        "cores": 1,
+        "cores": oracle.threads(0),
         "kind": "oracle",
         "sample": f"the full {wl.name} step (partition + local encode + round over all "
-                  f"{wl.P} elements), median of {reps} runs, single thread",
-        "s_per_step": round(t, 3),
+                  f"{wl.P} elements), median of {reps} runs on {all_threads} threads; "
+                  f"single thread: median of {max(1, min(reps, 3))}",
+        "s_per_step": round(tn, 3),
+        "single_thread": {"value": round(peer / t1 / 1e9, 4), "s_per_step": round(t1, 3)},
+        "threads_bit_identical": bool(same),
+        "build": "gcc -O3 -march=native -fopenmp -ffp-contract=off (static partition over elements)",
         "cpu_model": _cpu_model(),
+        "nproc": os.cpu_count(),
         "host_threads_available": len(os.sched_getaffinity(0)),
     }
 
 
 def _cpu_model():
+    """Model name of the host CPU with its family/model/stepping numbers."""
+    info = {}
     try:
         for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                return line.split(":", 1)[1].strip()
+            if ":" in line:
+                k, v = (a.strip() for a in line.split(":", 1))
+                if k in ("model name", "cpu family", "model", "stepping", "cache size") and k not in info:
+                    info[k] = v
+            elif info:
+                break
     except OSError:
-        pass
-    return None
+        return None
+    if "model name" not in info:
+        return None
+    return (f"{info['model name']} (family {info.get('cpu family')}, model {info.get('model')}, "
+            f"stepping {info.get('stepping')}, cache {info.get('cache size')})")
 
 
 def main():
@@ -521,6 +627,10 @@ def main():
 
     if args.mode == "balance":
         print(json.dumps(bench_balance()), flush=True)
+        return
+
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace, args.workload))
         return
 
     if args.summarize_counters:
@@ -595,6 +705,8 @@ def main():
     prof = D.dedloc_profile_end()
     kname, roof, per_kernel = kernel_roofline(dr, prof, args.steps)
     roof["traffic"], roof["traffic_source"] = measured_traffic(kname, wl.name)
+    roof["traffic_kind"] = ("FETCH_SIZE + WRITE_SIZE: bytes between the L2 caches and the fabric "
+                            "(Infinity Cache hits included, so not DRAM bytes), calibrated on a plain copy")
     if kname.endswith("fused_fp16") and not dr.local_in_kernel and roof["traffic"] is not None:
         # the committed counters were taken with the local peer's encode
         # inside this pass, which moves 4P more bytes
@@ -629,6 +741,20 @@ def main():
     ev1.record(stream)
     torch.cuda.synchronize()
     round_ms = ev0.elapsed_time(ev1) / args.steps
+
+    # the round alone, each call timed after the cache flush
+    flush = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    evs = []
+    for _ in range(args.steps):
+        torch.sum(flush, dim=0, out=sink)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        dr.call_round_only()
+        b.record(stream)
+        evs.append((a, b))
+    torch.cuda.synchronize()
+    round_cold_ms = sum(a.elapsed_time(b) for a, b in evs) / args.steps
+    del flush
 
     t = ms_per_step * 1e-3
     peer_bytes = dr.bytes_peer_input()
@@ -666,6 +792,9 @@ def main():
         "round_only": {"ms": round(round_ms, 5), "compulsory_bytes": dr.bytes_round(),
                        "algorithmic_frac_of_peak": round(dr.bytes_round() / (round_ms * 1e-3) / 1e9
                                                          / HBM_PEAK_GBPS, 4)},
+        "round_only_cold": {"ms": round(round_cold_ms, 5),
+                            "algorithmic_frac_of_peak": round(dr.bytes_round() / (round_cold_ms * 1e-3) / 1e9
+                                                              / HBM_PEAK_GBPS, 4)},
         "algorithmic_GBps": round(alg_bytes / t / 1e9, 2),
         "algorithmic_frac_of_peak": round(alg_bytes / t / 1e9 / HBM_PEAK_GBPS, 4),
         "roofline": roof,

@@ -47,6 +47,32 @@ def build(force: bool = True) -> str:
     return _LIB
 
 
+def build_fast(path: Optional[str] = None) -> str:
+    """The CPU baseline's build of the same source: -O3 for this host's CPU
+    (-march=native) with the OpenMP element loops on.  Still no contraction
+    and no fast-math, so every result is the same bits as the plain build,
+    for any thread count."""
+    path = path or os.path.join(_HERE, "liboracle_fast.so")
+    tmp = path + ".tmp"
+    subprocess.check_call(["gcc", "-O3", "-march=native", "-fopenmp", "-std=c11", "-fPIC", "-shared",
+                           "-ffp-contract=off", "-fno-fast-math",
+                           "-Wall", "-Wextra", "-Werror",
+                           _SRC, "-o", tmp, "-lm"])
+    os.replace(tmp, path)
+    return path
+
+
+def use_library(path: str) -> None:
+    """Call a given build of the oracle (for example build_fast()'s) from now on."""
+    global _LIB, _lib
+    _LIB, _lib = path, None
+
+
+def threads(n: int = 0) -> int:
+    """Threads of the OpenMP element loops (n > 0 sets them); 1 for the plain build."""
+    return int(_L().oracle_threads(n))
+
+
 class _LambCfg(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float),
                 ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
@@ -72,6 +98,7 @@ def _L():
         _lib = ctypes.CDLL(_LIB)
         vp, sz = ctypes.c_void_p, ctypes.c_size_t
         u32, u64 = ctypes.c_uint32, ctypes.c_uint64
+        _lib.oracle_threads.argtypes = [ctypes.c_int]
         _lib.oracle_partition.argtypes = [u64, u32, vp, u32, vp]
         _lib.oracle_weights.argtypes = [vp, u32, vp]
         _lib.oracle_encode_fp16.argtypes = [vp, sz, vp]

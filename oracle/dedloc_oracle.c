@@ -8,6 +8,11 @@
  *
  * Build: gcc -O2 -ffp-contract=off -fno-fast-math (no contraction: every fused
  * multiply-add below is an explicit fmaf, every other operation rounds once).
+ * The CPU baseline's build adds -O3 -march=native -fopenmp: loops marked
+ * OR_PARALLEL_FOR, whose iterations are independent, are then split
+ * statically over threads.  Every element is still computed by the same
+ * operations and every sum over elements stays sequential in element order,
+ * so the results are the same bits for any thread count.
  *
  * Pins (the checks that tie each function to something other than itself)
  * live in tests/test_oracle_*.py; the whole composed round is "parity
@@ -17,10 +22,28 @@
 #include <stddef.h>
 #include <stdint.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#define OR_PARALLEL_FOR _Pragma("omp parallel for schedule(static)")
+#else
+#define OR_PARALLEL_FOR
+#endif
 
 #define OR_OK 0
 #define OR_EINVAL (-1)
 #define OR_EZERO (-3)
+
+/* Threads the parallel loops use (n > 0 sets it); 1 in the plain build. */
+int oracle_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+    return omp_get_max_threads();
+#else
+    (void)n;
+    return 1;
+#endif
+}
 
 /* ------------------------------------------------------------------------ */
 /* Shard partition.  Section 3.2 / Appendix B: after solving the load-
@@ -121,11 +144,13 @@ static float f16_to_f32(uint16_t h)
 
 void oracle_encode_fp16(const float *x, size_t n, uint16_t *codes)
 {
+    OR_PARALLEL_FOR
     for (size_t i = 0; i < n; i++) codes[i] = f32_to_f16(x[i]);
 }
 
 void oracle_decode_fp16(const uint16_t *codes, size_t n, float *out)
 {
+    OR_PARALLEL_FOR
     for (size_t i = 0; i < n; i++) out[i] = f16_to_f32(codes[i]);
 }
 
@@ -139,7 +164,10 @@ void oracle_decode_fp16(const uint16_t *codes, size_t n, float *out)
 void oracle_encode_i8(const float *x, size_t n, uint32_t block, int8_t *codes,
                       float *scales)
 {
-    for (size_t b0 = 0, bi = 0; b0 < n; b0 += block, bi++) {
+    size_t nb = (n + block - 1) / block;
+    OR_PARALLEL_FOR
+    for (size_t bi = 0; bi < nb; bi++) {
+        size_t b0 = bi * block;
         size_t b1 = b0 + block < n ? b0 + block : n;
         float a = 0.0f;
         for (size_t i = b0; i < b1; i++) {
@@ -163,6 +191,7 @@ void oracle_encode_i8(const float *x, size_t n, uint32_t block, int8_t *codes,
 void oracle_decode_i8(const int8_t *codes, const float *scales, size_t n,
                       uint32_t block, float *out)
 {
+    OR_PARALLEL_FOR
     for (size_t i = 0; i < n; i++) out[i] = (float)codes[i] * scales[i / block];
 }
 
@@ -201,11 +230,13 @@ int oracle_reduce(const void *const *peer_codes, const float *const *peer_scales
     int rc = oracle_weights(counts, n_peers, w);
     if (rc != OR_OK) return rc;
     float *acc = scratch, *dec = scratch + len;
+    OR_PARALLEL_FOR
     for (size_t e = 0; e < len; e++) acc[e] = 0.0f;
     for (uint32_t p = 0; p < n_peers; p++) {
         if (counts[p] == 0) continue;
         decode_any(codec, peer_codes[p], peer_scales ? peer_scales[p] : NULL,
                    len, block, dec);
+        OR_PARALLEL_FOR
         for (size_t e = 0; e < len; e++) acc[e] = fmaf(w[p], dec[e], acc[e]);
     }
     if (out_mean) memcpy(out_mean, acc, len * sizeof(float));
@@ -248,8 +279,9 @@ int oracle_lamb(float *x, float *m, float *v, const float *g, uint64_t P,
     float omb1 = 1.0f - cfg->beta1, omb2 = 1.0f - cfg->beta2;
     for (uint32_t t = 0; t < T; t++) {
         float lam = (flags[t] & 1) ? cfg->weight_decay : 0.0f;
-        double sx = 0.0, su = 0.0;
-        for (uint64_t e = off[t]; e < off[t + 1]; e++) {
+        const uint64_t e0 = off[t], e1 = off[t + 1];
+        OR_PARALLEL_FOR
+        for (uint64_t e = e0; e < e1; e++) {
             float gg = g[e];
             float mn = fmaf(cfg->beta1, m[e], omb1 * gg);
             float vn = fmaf(cfg->beta2, v[e], omb2 * (gg * gg));
@@ -259,8 +291,11 @@ int oracle_lamb(float *x, float *m, float *v, const float *g, uint64_t P,
             m[e] = mn;
             v[e] = vn;
             u[e] = ue;
+        }
+        double sx = 0.0, su = 0.0;
+        for (uint64_t e = e0; e < e1; e++) {
             sx += (double)x[e] * (double)x[e];
-            su += (double)ue * (double)ue;
+            su += (double)u[e] * (double)u[e];
         }
         double X = sqrt(sx), U = sqrt(su);
         float r = 1.0f;
@@ -268,7 +303,8 @@ int oracle_lamb(float *x, float *m, float *v, const float *g, uint64_t P,
             r = (float)(X / U);
         if (trust) trust[t] = r;
         float lrr = cfg->lr * r;
-        for (uint64_t e = off[t]; e < off[t + 1]; e++) x[e] = x[e] - lrr * u[e];
+        OR_PARALLEL_FOR
+        for (uint64_t e = e0; e < e1; e++) x[e] = x[e] - lrr * u[e];
     }
     return OR_OK;
 }
@@ -308,7 +344,9 @@ int oracle_lars(float *x, float *v, const float *g, uint64_t P, const uint64_t *
             r = (float)((double)cfg->trust_coef * X / (G + (double)lam * X));
         if (trust) trust[t] = r;
         float s = cfg->lr * r;
-        for (uint64_t e = off[t]; e < off[t + 1]; e++) {
+        const uint64_t e0 = off[t], e1 = off[t + 1];
+        OR_PARALLEL_FOR
+        for (uint64_t e = e0; e < e1; e++) {
             float d = g[e] + lam * x[e];
             float vn = fmaf(cfg->momentum, v[e], s * d);
             v[e] = vn;

@@ -85,10 +85,10 @@ MUTANTS = [
     # The trust ratio's norms.  These two run with the float64 restatements of
     # LAMB deselected, so that a pin that does not restate the formula (the
     # hand-derived closed form with weight decay) has to catch them.
-    ("lamb: decay term left out of ||u||", "su += (double)ue * (double)ue;",
-     "su += (double)(ue - lam * x[e]) * (double)(ue - lam * x[e]);", NO_FLOAT64),
+    ("lamb: decay term left out of ||u||", "su += (double)u[e] * (double)u[e];",
+     "su += (double)(u[e] - lam * x[e]) * (double)(u[e] - lam * x[e]);", NO_FLOAT64),
     ("lamb: ||x - lr*u|| in place of ||x||", "sx += (double)x[e] * (double)x[e];\n            su",
-     "sx += (double)(x[e] - cfg->lr * ue) * (double)(x[e] - cfg->lr * ue);\n            su", NO_FLOAT64),
+     "sx += (double)(x[e] - cfg->lr * u[e]) * (double)(x[e] - cfg->lr * u[e]);\n            su", NO_FLOAT64),
 ]
 
 
