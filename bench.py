@@ -38,7 +38,7 @@ def _parse():
     ap.add_argument("--mode", default="round", choices=["round", "group", "balance", "accumulate"],
                     help="round: the averaging round (default); group: the group (Moshpit) "
                          "all-reduce of the workload's peer messages; balance: host solve time of "
-                         "the load-balancing LP for 4..32 peers; accumulate: the local peer's "
+                         "the load-balancing LP for 4..128 peers; accumulate: the local peer's "
                          "gradient accumulation and its overlap with the round")
     ap.add_argument("--group-size", type=int, default=8)
     ap.add_argument("--micro", type=int, default=8,
@@ -310,27 +310,36 @@ def measured_traffic(kernel, workload):
 
 
 def bench_balance():
-    """Host time of dedloc_balance (the library's simplex) and of the oracle
-    (HiGHS on the literal n^3-constraint program) on random collaborations:
-    compute 1..200 samples/s, bandwidths 10..1000 Mbit/s, ALBERT-large P."""
+    """Host time of dedloc_balance (the library's interior point; median of 5
+    solves after one warm-up) and of the oracle (HiGHS: the literal n^3
+    program up to 32 peers, its O(n^2) reformulation above) on random
+    collaborations: compute 1..200 samples/s, bandwidths 10..1000 Mbit/s,
+    ALBERT-large P."""
     from oracle import lp
     from paper_2106_10207_amd import dedloc as D
     rows = []
-    for n in (4, 8, 16, 24, 32):
+    for n in (4, 8, 16, 24, 32, 48, 64, 96, 128):
         rng = np.random.default_rng(n)
         s = rng.uniform(1, 200, n)
         d = rng.uniform(10, 1000, n) * 1e5 / 4
         u = rng.uniform(10, 1000, n) * 1e5 / 4
         B, P = 4096.0, 17_683_968.0
-        t0 = time.perf_counter()
         r = D.dedloc_balance(s, d, u, B, P)
+        times = []
+        for _ in range(5):
+            t0 = time.perf_counter()
+            r = D.dedloc_balance(s, d, u, B, P)
+            times.append(time.perf_counter() - t0)
+        reduced = n > 32
         t1 = time.perf_counter()
-        o = lp.solve(s, d, u, B, P)
+        o = lp.solve(s, d, u, B, P, reduced=reduced)
         t2 = time.perf_counter()
-        rows.append({"peers": n, "lib_ms": round((t1 - t0) * 1e3, 2), "oracle_ms": round((t2 - t1) * 1e3, 1),
+        rows.append({"peers": n, "lib_ms": round(float(np.median(times)) * 1e3, 2),
+                     "oracle_ms": round((t2 - t1) * 1e3, 1), "oracle_program": "reduced" if reduced else "literal",
                      "xi": r["xi"], "xi_oracle": o["xi"]})
+        print(json.dumps(rows[-1]), file=sys.stderr, flush=True)
     return {"metric": "load-balancing LP solve time (host)", "unit": "ms", "higher_is_better": False,
-            "cores": 1, "rows": rows}
+            "cores": 1, "cpu_model": _cpu_model(), "rows": rows}
 
 
 def bench_group(args, wl):

@@ -372,23 +372,35 @@ int dedloc_finalize(float *acc, uint64_t n, uint32_t count, int32_t codec, uint3
  *   g_ij <= a_ki + (1 - c_k) d_i                               (every i, j, k)
  *   sum_{j != i} (a_ji + g_ji) <= d_i;  sum_{j != i} (a_ij + g_ij) <= u_i
  *   a_ij + g_ij <= t_ij (where finite);  a, g >= 0;  0 <= c <= 1
- * solved on the host by a deterministic dense simplex (the n^3 aggregation
- * constraints are replaced by an exactly equivalent O(n^2) set with a rate
- * variable per reducer).  Reducer i's share is proportional to min_{j != i}
- * g_ij (the appendix's "fraction" equation; the rate to itself is free).
+ * solved on the host by a deterministic primal-dual interior-point method
+ * (the appendix also solves it with one).  The n^3 aggregation constraints
+ * are replaced by an exactly equivalent O(n^2) set with a rate variable per
+ * reducer; each Newton system is reduced to a dense symmetric system of
+ * about 5n unknowns (Bunch-Kaufman LDL^T).  Converged to a relative duality
+ * gap of 1e-12 (an iterate within 1e-9 on every measure is accepted if
+ * rounding stalls it earlier).  Equal inputs give equal outputs bit for bit.
+ * Reducer i's share is proportional to min_{j != i} g_ij (the appendix's
+ * "fraction" equation; the rate to itself is free).
  * Units: s in samples/s, d, u, t in parameters/s, B samples, P parameters.
  * Peers with can_aggregate[i] == 0 receive nothing to aggregate (a_ji = g_ij
- * = 0).  All arrays are host memory; t (n*n, row-major, INFINITY = no limit)
- * and can_aggregate may be NULL.
+ * = 0).  c_fixed (nullable, n entries): c_i is fixed to c_fixed[i] in [0, 1]
+ * where it is not NaN (1 and 0 give the paper's binary choice before the
+ * relaxation: the parameter-server and BytePS special cases of Section 3.2).
+ * All arrays are host memory; t (n*n, row-major, INFINITY = no limit),
+ * can_aggregate and c_fixed may be NULL.
  * Outputs: xi, c[n], frac[n] (sums to 1), weights[n] (nullable): frac scaled
  * to integers summing to about 2^24, ready for dedloc_partition; a[n*n] and
- * g[n*n] (nullable) in parameters/s.  n <= DEDLOC_BALANCE_MAX_PEERS. */
-#define DEDLOC_BALANCE_MAX_PEERS 32
+ * g[n*n] (nullable) in parameters/s.  n <= DEDLOC_BALANCE_MAX_PEERS.
+ * Errors: NULL required arrays, n out of range, B or P not positive, a
+ * negative or non-finite s, d, u, a negative or NaN t, c_fixed outside
+ * [0, 1] -> INVALID_ARG; no convergence -> INVALID_ARG. */
+#define DEDLOC_BALANCE_MAX_PEERS 128
 typedef struct {
     uint32_t n;
     const double *s, *d, *u, *t;
     const uint8_t *can_aggregate;
     double B, P;
+    const double *c_fixed;
 } dedloc_balance_problem;
 int dedloc_balance(const dedloc_balance_problem *pr, double *xi, double *c, double *frac,
                    uint64_t *weights, double *a, double *g);

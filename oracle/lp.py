@@ -36,10 +36,19 @@ def _idx(n):
     return a, g, c, xi, 2 * n * n + n + 1
 
 
-def solve(s, d, u, B, P, t=None, can_aggregate=None, fix_c=None):
+def solve(s, d, u, B, P, t=None, can_aggregate=None, fix_c=None, reduced=False):
     """Solve the relaxed LP.  Returns dict(xi, a, g, c, frac, status).
 
     fix_c: optional array; where not NaN, c_i is fixed to that value.
+
+    reduced: replace the n^3 aggregation rows g_ij <= a_ki + (1 - c_k) d_i by
+    the 2n^2 rows  g_ij <= h_i  and  h_i <= a_ki + (1 - c_k) d_i  with one
+    more variable h_i per peer (its aggregation rate).  The two programs have
+    the same feasible set in (a, g, c, xi): h_i = max_j g_ij turns a point of
+    the first into one of the second, and the second's rows chain into the
+    first's.  Only the literal program is the oracle's definition; the
+    reduced one exists because HiGHS needs minutes on the literal one past
+    ~40 peers, and it is pinned against the literal one in the tests.
 
     Rates are handed to the solver in whole vectors per second (bandwidths
     divided by P, and P = 1): the same program in other units.  Left in
@@ -57,6 +66,10 @@ def solve(s, d, u, B, P, t=None, can_aggregate=None, fix_c=None):
     Pu = P
     P = 1.0
     a, g, c, xi, nv = _idx(n)
+    h0 = nv
+    h = lambda i: h0 + i
+    if reduced:
+        nv += n
     rows, cols, vals, rhs = [], [], [], []
     r = 0
 
@@ -72,10 +85,17 @@ def solve(s, d, u, B, P, t=None, can_aggregate=None, fix_c=None):
     add([(xi, 1.0)] + [(c(i), -s[i] / B) for i in range(n)], 0.0)
     for i in range(n):
         add([(xi, 1.0)] + [(g(j, i), -1.0 / P) for j in range(n)], 0.0)
-    for i in range(n):
-        for j in range(n):
+    if reduced:
+        for i in range(n):
+            for j in range(n):
+                add([(g(i, j), 1.0), (h(i), -1.0)], 0.0)
             for k in range(n):
-                add([(g(i, j), 1.0), (a(k, i), -1.0), (c(k), d[i])], d[i])
+                add([(h(i), 1.0), (a(k, i), -1.0), (c(k), d[i])], d[i])
+    else:
+        for i in range(n):
+            for j in range(n):
+                for k in range(n):
+                    add([(g(i, j), 1.0), (a(k, i), -1.0), (c(k), d[i])], d[i])
     for i in range(n):
         add([(a(j, i), 1.0) for j in range(n) if j != i] + [(g(j, i), 1.0) for j in range(n) if j != i], d[i])
         add([(a(i, j), 1.0) for j in range(n) if j != i] + [(g(i, j), 1.0) for j in range(n) if j != i], u[i])
@@ -86,7 +106,7 @@ def solve(s, d, u, B, P, t=None, can_aggregate=None, fix_c=None):
                 if np.isfinite(t[i, j]):
                     add([(a(i, j), 1.0), (g(i, j), 1.0)], t[i, j])
     A = sp.csr_matrix((vals, (rows, cols)), shape=(r, nv))
-    bounds = [(0, None)] * (2 * n * n) + [(0, 1)] * n + [(None, None)]
+    bounds = [(0, None)] * (2 * n * n) + [(0, 1)] * n + [(None, None)] + [(0, None)] * (n if reduced else 0)
     if can_aggregate is not None:
         for i in range(n):
             if not can_aggregate[i]:

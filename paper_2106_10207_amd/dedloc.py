@@ -30,6 +30,7 @@ DEDLOC_CODEC_FP16 = 1
 DEDLOC_CODEC_I8 = 2
 DEDLOC_I8_BLOCK = 1024
 DEDLOC_NOALLOC_SCRATCH_BYTES = 16 << 20  # static workspace of dedloc_round_noalloc
+DEDLOC_BALANCE_MAX_PEERS = 128
 DEDLOC_MAX_PEERS = 1024
 DEDLOC_MAX_GROUP_PEERS = 1024
 DEDLOC_MAX_GROUP_SIZE = 64
@@ -78,7 +79,7 @@ class dedloc_local_peer(ctypes.Structure):
 class dedloc_balance_problem(ctypes.Structure):
     _fields_ = [("n", ctypes.c_uint32), ("s", ctypes.c_void_p), ("d", ctypes.c_void_p),
                 ("u", ctypes.c_void_p), ("t", ctypes.c_void_p), ("can_aggregate", ctypes.c_void_p),
-                ("B", ctypes.c_double), ("P", ctypes.c_double)]
+                ("B", ctypes.c_double), ("P", ctypes.c_double), ("c_fixed", ctypes.c_void_p)]
 
 
 _lib = None
@@ -560,14 +561,21 @@ def dedloc_finalize(acc, count: int, codec: int, block: int = DEDLOC_I8_BLOCK, c
     return codes, scales
 
 
-def dedloc_balance(s, d, u, B: float, P: float, t=None, can_aggregate=None):
+def dedloc_balance(s, d, u, B: float, P: float, t=None, can_aggregate=None, c_fixed=None):
     """Solve the load-balancing LP on the host.  Returns dict(xi, c, frac,
-    weights, a, g) (rates in parameters/s)."""
+    weights, a, g) (rates in parameters/s).  c_fixed: optional per-peer
+    compute indicators (NaN = free)."""
     s, d, u = (_host(v, np.float64) for v in (s, d, u))
     n = s.size
+    for name, v in (("d", d), ("u", u)):
+        if v.size != n:
+            raise ValueError(f"{name} has {v.size} entries, s has {n}")
     tt = None if t is None else _host(t, np.float64).reshape(n * n)
     ca = None if can_aggregate is None else _host(can_aggregate, np.uint8)
-    pr = dedloc_balance_problem(n, _ptr(s), _ptr(d), _ptr(u), _ptr(tt), _ptr(ca), B, P)
+    cf = None if c_fixed is None else _host(c_fixed, np.float64)
+    if ca is not None and ca.size != n or cf is not None and cf.size != n:
+        raise ValueError("can_aggregate and c_fixed need one entry per peer")
+    pr = dedloc_balance_problem(n, _ptr(s), _ptr(d), _ptr(u), _ptr(tt), _ptr(ca), B, P, _ptr(cf))
     xi = ctypes.c_double(0.0)
     c = np.zeros(n)
     frac = np.zeros(n)

@@ -1,9 +1,14 @@
-"""The library's load balancer (dedloc_balance, host C++ simplex) against the
-oracle's LP (Appendix B's program written out literally, solved by HiGHS).
+"""The library's load balancer (dedloc_balance, host C++ interior point)
+against the oracle's LP (Appendix B's program written out literally, solved by
+HiGHS; from 32 peers on with regional limits, and at 48 and 64 peers, the
+oracle's O(n^2) reformulation, pinned against the literal program in
+tests/test_oracle_lp.py, because HiGHS needs minutes on the literal one).
 
 The optimum xi is unique and must agree; optimal points need not be unique,
 so the library's own (a, g, c) is checked for feasibility in the original
-n^3-constraint program, and its shares are recomputed from its g."""
+n^3-constraint program, and its shares are recomputed from its g.  Section
+3.2's parameter-server and BytePS cases are checked against their closed
+forms with the compute indicators fixed to the binary choice."""
 
 import numpy as np
 import pytest
@@ -28,8 +33,8 @@ def _problem(n, seed, regional=False, aux=False):
     return s, d, u, t
 
 
-def _check(r, s, d, u, B, P, t=None, agg=None):
-    o = lp.solve(s, d, u, B, P, t=t, can_aggregate=agg)
+def _check(r, s, d, u, B, P, t=None, agg=None, reduced=False):
+    o = lp.solve(s, d, u, B, P, t=t, can_aggregate=agg, reduced=reduced)
     assert np.isclose(r["xi"], o["xi"], rtol=1e-9, atol=0), (r["xi"], o["xi"])
     sol = dict(a=r["a"], g=r["g"], c=r["c"], xi=r["xi"])
     assert lp.violation(sol, s, d, u, B, P, t=t, can_aggregate=agg) < 1e-9
@@ -40,13 +45,54 @@ def _check(r, s, d, u, B, P, t=None, agg=None):
     return o
 
 
-@pytest.mark.parametrize("n", [1, 2, 3, 5, 8, 12, 16])
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 8, 12, 16, 24, 32, 48, 64])
 @pytest.mark.parametrize("variant", ["plain", "aux", "regional"])
 def test_matches_oracle(n, variant):
     s, d, u, t = _problem(n, 1000 * n + len(variant), regional=variant == "regional", aux=variant == "aux")
     B, P = 4096.0, 17_683_968.0
     r = D.dedloc_balance(s, d, u, B, P, t=t)
-    _check(r, s, d, u, B, P, t=t)
+    # the literal n^3 program up to 32 peers (regional limits: up to 24)
+    reduced = n > 32 or (n == 32 and variant == "regional")
+    _check(r, s, d, u, B, P, t=t, reduced=reduced)
+
+
+@pytest.mark.parametrize("n", [2, 4, 8])
+def test_parameter_server_case(n):
+    """One peer without compute and with bandwidth for everyone takes the
+    whole aggregation; each worker then runs at its link's rate b/P."""
+    b, P = 1e6, 1e6
+    s = np.array([1e9] * n + [0.0])
+    bw = np.array([b] * n + [2 * n * b])
+    r = D.dedloc_balance(s, bw, bw, 1.0, P, c_fixed=np.array([1.0] * n + [0.0]))
+    assert np.isclose(r["xi"], b / P, rtol=1e-9)
+    assert np.allclose(r["frac"], [0.0] * n + [1.0], atol=1e-7)
+    assert np.array_equal(r["c"], [1.0] * n + [0.0])
+
+
+def test_byteps_case():
+    """8 workers and 8 summation peers of equal bandwidth: 12/19 b/P (the
+    workers alone: 4/7 b/P), the summation peers aggregating."""
+    b, P = 1e6, 1e6
+    s = np.array([1e9] * 8 + [0.0] * 8)
+    bw = np.full(16, b)
+    cf = np.array([1.0] * 8 + [0.0] * 8)
+    r = D.dedloc_balance(s, bw, bw, 1.0, P, c_fixed=cf)
+    assert np.isclose(r["xi"], 12.0 / 19.0 * b / P, rtol=1e-9)
+    assert r["frac"][8:].sum() > 0.5
+    o = lp.solve(s, bw, bw, 1.0, P, fix_c=cf)
+    assert np.isclose(r["xi"], o["xi"], rtol=1e-9)
+
+
+@pytest.mark.parametrize("n", [5, 12])
+def test_fixed_compute_matches_oracle(n):
+    s, d, u, _ = _problem(n, 77 + n)
+    cf = np.where(np.arange(n) % 3 == 0, np.nan, np.where(np.arange(n) % 3 == 1, 1.0, 0.25))
+    B, P = 4096.0, 17_683_968.0
+    r = D.dedloc_balance(s, d, u, B, P, c_fixed=cf)
+    o = lp.solve(s, d, u, B, P, fix_c=cf)
+    assert np.isclose(r["xi"], o["xi"], rtol=1e-9)
+    fixed = ~np.isnan(cf)
+    assert np.array_equal(r["c"][fixed], cf[fixed])
 
 
 def test_non_aggregators():
@@ -82,14 +128,19 @@ def test_deterministic_and_partition():
     assert np.all(np.abs(sizes - r1["frac"] * P) <= 64 + P * 1e-6)
 
 
-@pytest.mark.parametrize("bad", ["n0", "n33", "B", "neg"])
+@pytest.mark.parametrize("bad", ["n0", "n_max", "B", "neg", "inf", "c_fixed"])
 def test_rejects(bad):
-    n = 33 if bad == "n33" else 3
+    n = D.DEDLOC_BALANCE_MAX_PEERS + 1 if bad == "n_max" else 3
     s, d, u = np.ones(n), np.ones(n), np.ones(n)
     B = 0.0 if bad == "B" else 1.0
+    cf = None
     if bad == "neg":
         d[1] = -1.0
+    if bad == "inf":
+        u[2] = np.inf
+    if bad == "c_fixed":
+        cf = np.array([np.nan, 1.5, 0.0])
     if bad == "n0":
         s, d, u = np.ones(0), np.ones(0), np.ones(0)
     with pytest.raises(D.DedlocError):
-        D.dedloc_balance(s, d, u, B, 1.0)
+        D.dedloc_balance(s, d, u, B, 1.0, c_fixed=cf)

@@ -12,7 +12,16 @@ builds:
   of the relaxed LP, which the binary problem cannot reach);
 * the relaxation bounds every binary choice of c from above (brute force
   over c in {0,1}^n, n <= 4);
-* the returned solution satisfies every constraint, and its shares sum to 1."""
+* the returned solution satisfies every constraint, and its shares sum to 1;
+* Section 3.2's special cases, with the compute indicators fixed to the
+  binary choice the relaxation stands for (closed forms derived by hand):
+  a parameter server (one peer with no compute and bandwidth for everyone)
+  takes the whole aggregation and every worker then runs at its own
+  bandwidth, xi = b/P; BytePS-style summation peers (no compute, the
+  workers' bandwidth) raise 8 workers from the all-reduce rate 4/7*b/P to
+  12/19*b/P and necessarily aggregate;
+* the O(n^2) reformulation used for large collaborations has the literal
+  program's optimum."""
 
 import itertools
 
@@ -95,3 +104,67 @@ def test_regional_limits_and_non_aggregators():
     assert r["frac"][2] == 0.0 and np.isclose(r["frac"].sum(), 1.0)
     free = lp.solve(s, d, u, 2048.0, 5e6)
     assert r["xi"] <= free["xi"] * (1 + 1e-9)
+
+
+@pytest.mark.parametrize("n", [2, 3, 4, 8])
+def test_parameter_server(n):
+    """Section 3.2: one peer with a very high bandwidth and no compute turns
+    the collaboration into a parameter server.  Workers (c = 1) must each send
+    their gradient to every aggregator at its rate, so worker k's upload
+    carries h_PS + sum_{i != k} h_i + n h_k <= b while every peer receives
+    h_PS + sum_i h_i; summed over the workers, xi*P <= b - (n-1)/n * H with H
+    the workers' total aggregation: the optimum has H = 0, the server takes
+    the whole vector (share 1) and xi = b/P, each worker's link saturated."""
+    b, P = 1e6, 1e6
+    s = np.array([1e9] * n + [0.0])
+    bw = np.array([b] * n + [2 * n * b])
+    r = lp.solve(s, bw, bw, B=1.0, P=P, fix_c=np.array([1.0] * n + [0.0]))
+    assert np.isclose(r["xi"], b / P, rtol=1e-9)
+    assert np.allclose(r["frac"], [0.0] * n + [1.0], atol=1e-9)
+    if n > 2:  # better than the workers' own all-reduce
+        assert r["xi"] > n * b / (2 * (n - 1) * P) * 1.01
+
+
+def test_byteps_summation_peers():
+    """Section 3.2: peers with the workers' bandwidth and no compute act as
+    BytePS summation servers.  8 workers (c = 1) and 8 such peers (c = 0), all
+    with bandwidth b; in a symmetric optimum (which exists: the program is
+    convex and symmetric) a worker aggregates h_w and a summation peer h_a,
+    and the binding constraints are the worker's upload, 22 h_w + 8 h_a <= b,
+    and the summation peer's download, 8 h_w + 15 h_a <= b: h_w = b/38,
+    h_a = b/19, xi*P = 8 (h_w + h_a) = 12/19 b, against 4/7 b for the
+    workers' all-reduce alone.  Without the summation peers aggregating,
+    every worker would also have to send the average to them, capping xi*P
+    at 8/22 b: so they do aggregate."""
+    b, P = 1e6, 1e6
+    s = np.array([1e9] * 8 + [0.0] * 8)
+    bw = np.full(16, b)
+    r = lp.solve(s, bw, bw, B=1.0, P=P, fix_c=np.array([1.0] * 8 + [0.0] * 8))
+    assert np.isclose(r["xi"], 12.0 / 19.0 * b / P, rtol=1e-9)
+    assert r["xi"] > 4.0 / 7.0 * b / P
+    assert r["frac"][8:].sum() > 0.0
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 8, 12])
+@pytest.mark.parametrize("variant", ["plain", "fixed", "regional", "no_agg"])
+def test_reduced_form_has_the_literal_optimum(n, variant):
+    rng = np.random.default_rng(100 * n + len(variant))
+    s = rng.uniform(1, 200, n)
+    d = rng.uniform(10, 1000, n) * 2.5e4
+    u = rng.uniform(10, 1000, n) * 2.5e4
+    kw = {}
+    if variant == "fixed":
+        kw["fix_c"] = np.where(rng.uniform(size=n) < 0.5, 1.0, np.nan)
+    if variant == "regional":
+        t = np.full((n, n), np.inf)
+        for _ in range(n):
+            i, j = rng.integers(0, n, 2)
+            t[i, j] = rng.uniform(1, 50) * 2.5e4
+        kw["t"] = t
+    if variant == "no_agg":
+        kw["can_aggregate"] = rng.uniform(size=n) < 0.7
+    lit = lp.solve(s, d, u, 4096.0, 2e7, **kw)
+    red = lp.solve(s, d, u, 4096.0, 2e7, reduced=True, **kw)
+    assert lit["status"] == 0 and red["status"] == 0
+    assert np.isclose(red["xi"], lit["xi"], rtol=1e-9, atol=1e-15)
+    assert lp.violation(red, s, d, u, 4096.0, 2e7, t=kw.get("t"), can_aggregate=kw.get("can_aggregate")) < 1e-9

@@ -108,6 +108,10 @@ LP_MUTANTS = [
      "add([(a(i, j), 1.0) for j in range(n) if j != i] + [(g(i, j), 1.0) for j in range(n) if j != i], u[i])",
      "add([(a(i, j), 1.0) for j in range(n)] + [(g(i, j), 1.0) for j in range(n)], u[i])"),
     ("lp: c unbounded above", "[(0, 1)] * n", "[(0, None)] * n"),
+    ("lp: a peer's own share not counted in what it receives", "[(g(j, i), -1.0 / P) for j in range(n)]",
+     "[(g(j, i), -1.0 / P) for j in range(n) if j != i]"),
+    ("lp: reduced form without the aggregation rate bound", "add([(g(i, j), 1.0), (h(i), -1.0)], 0.0)",
+     "add([(g(i, j), 1.0), (h(i), -0.5)], 0.0)"),
 ]
 
 
