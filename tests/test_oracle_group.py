@@ -8,7 +8,10 @@ ceil(log_m n) iterations).
 * one iteration fewer does not reach it (peers in different groups still
   disagree by far more than the rounding);
 * peers of the same final group hold the same message; zero-sample peers
-  and the empty slots of an incomplete grid change nothing."""
+  and the empty slots of an incomplete grid change nothing;
+* groups of m = 2 (Section 3.2's decentralized-SGD case): every iteration
+  averages disjoint pairs of peers, and after the first one each pair holds
+  exactly what the plain reducer makes of the two messages."""
 
 import numpy as np
 import pytest
@@ -113,3 +116,28 @@ def test_errors():
         oracle.group_allreduce(codes, [0, 0, 0], 2, oracle.CODEC_FP16)
     with pytest.raises(oracle.OracleError):
         oracle.group_allreduce(codes, [1, 1, 1], 1, oracle.CODEC_FP16)
+
+
+@pytest.mark.parametrize("codec", [oracle.CODEC_FP16, oracle.CODEC_I8])
+def test_group_size_two_is_pairwise_gossip(codec):
+    """Section 3.2: with m = 2 all communication happens between pairs of
+    nodes, as in D-PSGD.  Iteration 1 groups the slots that differ in the
+    lowest base-2 digit: peers 2g and 2g+1 both end with the pair's
+    sample-weighted average, which is the plain reducer on those two
+    messages (a peer without samples contributes nothing)."""
+    n, L = 8, 3000
+    _, codes, scales = _msgs(n, L, 5, codec, spread=True)
+    counts = np.array([3, 9, 1, 1, 0, 4, 7, 2], np.uint32)
+    out, osc, peer_out = oracle.group_allreduce(codes, counts, 2, codec, scales, iters=1)
+    assert out.shape[0] == n // 2
+    for g in range(n // 2):
+        pair = [2 * g, 2 * g + 1]
+        rc, rs, _ = oracle.reduce([codes[i] for i in pair], counts[pair], codec,
+                                  None if scales is None else [scales[i] for i in pair])
+        assert np.array_equal(out[g], rc), g
+        if codec == oracle.CODEC_I8:
+            assert np.array_equal(osc[g], rs), g
+        assert peer_out[2 * g] == peer_out[2 * g + 1] == g
+    # pairs are still far apart after one iteration: gossip, not yet the average
+    dec = [_dec(codec, out[g], None if osc is None else osc[g]) for g in range(n // 2)]
+    assert np.max(np.abs(dec[0] - dec[3])) > 1e-3
