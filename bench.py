@@ -765,6 +765,15 @@ def main():
     round_cold_ms = sum(a.elapsed_time(b) for a, b in evs) / args.steps
     del flush
 
+    # the round's own compulsory bytes over the round alone, warm and cold:
+    # the figures the 70% target is about (the kernel figure above is the
+    # dominant pass's)
+    roof["round"] = {
+        "compulsory_bytes": dr.bytes_round(),
+        "frac_warm": round(dr.bytes_round() / (round_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+        "frac_cold": round(dr.bytes_round() / (round_cold_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+    }
+
     t = ms_per_step * 1e-3
     peer_bytes = dr.bytes_peer_input()
     alg_bytes = dr.bytes_step()
