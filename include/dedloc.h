@@ -405,6 +405,24 @@ typedef struct {
 int dedloc_balance(const dedloc_balance_problem *pr, double *xi, double *c, double *frac,
                    uint64_t *weights, double *a, double *g);
 
+/* Group size for dedloc_group_allreduce (Appendix C "Fault tolerance"):
+ * the m in [2, min(n_peers, max_group)] that minimises the expected number
+ * of iterations to the global average, counting restarts after failures:
+ *     E(m) = ceil(log_m n_peers) / (1 - failure_rate)^m,
+ * with failure_rate the probability that one peer fails during one group
+ * attempt (a group of m succeeds only if none of its members fails, and
+ * restarts otherwise).  The paper states the objective but no formula; this
+ * reading reaches the two limits it does state: m = n when failures are
+ * rare, m = 2 (pairs, as in decentralized SGD; Section 3.2) when they are
+ * frequent.  Ties go to the smaller m.  Host-only.
+ *   n_peers in [2, DEDLOC_MAX_GROUP_PEERS], 0 <= failure_rate < 1,
+ *   max_group = 0 (no cap) or >= 2; otherwise INVALID_ARG.
+ *   m_out: host, required; expected_out: host, nullable (E of the chosen m).
+ * dedloc_group_allreduce takes groups of at most DEDLOC_MAX_GROUP_SIZE:
+ * pass that as max_group to get a size it accepts. */
+int dedloc_group_size(uint32_t n_peers, double failure_rate, uint32_t max_group, uint32_t *m_out,
+                      double *expected_out);
+
 /* Per-kernel timing (tracing support for benchmarks).  Between
  * dedloc_profile_begin() and dedloc_profile_end() every kernel the library
  * enqueues is bracketed by a pair of HIP events on its stream; at most

@@ -16,6 +16,8 @@ Functions and the passages they follow:
   round_lars - the same round with the LARS step
   group_allreduce - Section 3.2 "Node failures" / Appendix C (group averaging)
   accumulate/finalize - Section 3.1 (local accumulation to the target batch)
+  lp (module)     - Appendix B (the load-balancing LP, solved by HiGHS)
+  groups (module) - Appendix C (the group size of the group all-reduce)
 """
 
 from __future__ import annotations

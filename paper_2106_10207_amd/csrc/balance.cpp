@@ -827,3 +827,31 @@ extern "C" int dedloc_balance(const dedloc_balance_problem *pr, double *xi_out, 
         for (int i = 0; i < n * n; i++) g_out[i] = vg[i] >= 0 ? x[vg[i]] * P : 0.0;
     return DEDLOC_OK;
 }
+
+// Group size of the group all-reduce (Appendix C): the m minimising
+// ceil(log_m n) / (1 - p)^m, as declared in dedloc.h.
+extern "C" int dedloc_group_size(uint32_t n_peers, double failure_rate, uint32_t max_group, uint32_t *m_out,
+                                 double *expected_out) {
+    if (!m_out || n_peers < 2 || n_peers > DEDLOC_MAX_GROUP_PEERS || !(failure_rate >= 0.0) ||
+        !(failure_rate < 1.0) || max_group == 1)
+        return DEDLOC_ERR_INVALID_ARG;
+    const uint32_t hi = max_group ? std::min(max_group, n_peers) : n_peers;
+    uint32_t best_m = 0;
+    double best = INFINITY;
+    for (uint32_t m = 2; m <= hi; m++) {
+        uint32_t d = 1;
+        uint64_t reach = m;
+        while (reach < n_peers) {
+            reach *= m;
+            d++;
+        }
+        const double e = (double)d / pow(1.0 - failure_rate, (double)m);
+        if (e < best) {
+            best = e;
+            best_m = m;
+        }
+    }
+    *m_out = best_m;
+    if (expected_out) *expected_out = best;
+    return DEDLOC_OK;
+}

@@ -136,6 +136,8 @@ _SIGS = {
                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p], ctypes.c_int),
     "dedloc_balance": ([ctypes.POINTER(dedloc_balance_problem), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
+    "dedloc_group_size": ([ctypes.c_uint32, ctypes.c_double, ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p],
+                          ctypes.c_int),
     "dedloc_profile_begin": ([ctypes.c_uint32], ctypes.c_int),
     "dedloc_profile_end": ([ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "dedloc_kernel_kinds": ([], ctypes.c_int),
@@ -475,6 +477,18 @@ def dedloc_round_lars(peer_codes, counts, bounds, codec: int, x, v, offsets, fla
     RoundCall(peer_codes, counts, bounds, codec, out_codes, x, None, v, offsets, flags, cfg, ws, peer_scales,
               out_scales, trust_out, out_mean, block, local)(stream)
     return out_codes, out_scales
+
+
+def dedloc_group_size(n_peers: int, failure_rate: float, max_group: int = 0):
+    """(m, expected iterations) of the group size minimising the expected
+    iterations to the global average (dedloc.h)."""
+    m = ctypes.c_uint32(0)
+    e = ctypes.c_double(0.0)
+    lib = load()
+    rc = lib.dedloc_group_size(n_peers, failure_rate, max_group, ctypes.byref(m), ctypes.byref(e))
+    if rc != DEDLOC_OK:
+        raise DedlocError(rc, "dedloc_group_size: n_peers in [2, 1024], 0 <= failure_rate < 1, max_group 0 or >= 2")
+    return m.value, e.value
 
 
 def group_iterations(n_peers: int, group_size: int) -> int:

@@ -144,3 +144,20 @@ def test_rejects(bad):
         s, d, u = np.ones(0), np.ones(0), np.ones(0)
     with pytest.raises(D.DedlocError):
         D.dedloc_balance(s, d, u, B, 1.0, c_fixed=cf)
+
+
+@pytest.mark.parametrize("n", [2, 3, 8, 16, 64, 100, 300, 1024])
+@pytest.mark.parametrize("p", [0.0, 1e-4, 0.003, 0.02, 0.1, 0.4, 0.95])
+def test_group_size_matches_oracle(n, p):
+    from oracle import groups
+    m, e = D.dedloc_group_size(n, p)
+    om, oe = groups.optimal_group_size(n, p)
+    assert m == om and np.isclose(e, oe, rtol=1e-12)
+    cm, ce = D.dedloc_group_size(n, p, max_group=D.DEDLOC_MAX_GROUP_SIZE)
+    assert (cm, ce) == groups.optimal_group_size(n, p, D.DEDLOC_MAX_GROUP_SIZE)
+
+
+def test_group_size_rejects():
+    for args in ((1, 0.1), (2, 1.0), (2, -0.1), (1025, 0.0), (4, 0.1, 1)):
+        with pytest.raises(D.DedlocError):
+            D.dedloc_group_size(*args)
