@@ -17,6 +17,7 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "dedloc_oracle.c")
+_WORKERS = max(1, min(6, (os.cpu_count() or 2) - 1))
 
 # pytest -k expression that leaves out the tests built on a float64
 # restatement of the LAMB formula
@@ -128,13 +129,20 @@ def _lp_pins_on(src_path):
     return r.returncode
 
 
+# test files that are not pins of the C oracle: this file, the comparison of
+# the oracle's two builds with each other (a mutant agrees with itself), and
+# the pure-Python LP and group-size modules
+_NOT_C_PINS = (os.path.basename(__file__), "test_oracle_fast_build.py", "test_oracle_lp.py",
+               "test_oracle_group_size.py")
+
+
 def _pins_on(lib_path, kexpr=None):
     k = ['-k', kexpr] if kexpr else []
-    code = ("import sys, oracle\n"
+    code = ("import os, sys, oracle\n"
             f"oracle._LIB = {lib_path!r}\n"
             "import pytest, glob\n"
             "files = sorted(glob.glob('tests/test_oracle_*.py'))\n"
-            f"files = [f for f in files if not f.endswith({os.path.basename(__file__)!r})]\n"
+            f"files = [f for f in files if os.path.basename(f) not in {_NOT_C_PINS!r}]\n"
             f"sys.exit(pytest.main(['-x', '-q', '-p', 'no:cacheprovider', '-m', 'not gpu'] + {k!r} + files))\n")
     r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True, timeout=600)
     return r.returncode
@@ -154,7 +162,7 @@ def _mutant(i, name, old, new, tmp, kexpr=None):
 def test_pins_catch_every_mutant(tmp_path):
     assert _pins_on(os.path.join(ROOT, "oracle", "liboracle.so")) == 0  # the real oracle passes
     assert _pins_on(os.path.join(ROOT, "oracle", "liboracle.so"), NO_FLOAT64) == 0
-    with concurrent.futures.ThreadPoolExecutor(max_workers=4) as ex:
+    with concurrent.futures.ThreadPoolExecutor(max_workers=_WORKERS) as ex:
         results = list(ex.map(lambda a: _mutant(a[0], *a[1][:3], str(tmp_path), *a[1][3:]), enumerate(MUTANTS)))
     survivors = [name for name, rc in results if rc == 0]
     assert not survivors, f"mutants the pins do not catch: {survivors}"
@@ -171,7 +179,7 @@ def test_lp_pins_catch_every_mutant(tmp_path):
         open(path, "w").write(src.replace(old, new))
         return name, _lp_pins_on(path)
 
-    with concurrent.futures.ThreadPoolExecutor(max_workers=4) as ex:
+    with concurrent.futures.ThreadPoolExecutor(max_workers=_WORKERS) as ex:
         results = list(ex.map(lambda a: run(a[0], *a[1]), enumerate(LP_MUTANTS)))
     survivors = [name for name, rc in results if rc == 0]
     assert not survivors, f"LP mutants the pins do not catch: {survivors}"
