@@ -195,6 +195,32 @@ def test_round_many_chunks(codec, opt):
                       counts=counts, local=2, grads=grads, bounds=bounds, x=x, m=m, v=v, cfg=cfg))
 
 
+@pytest.mark.parametrize("n_peers", [3, 9, 70])
+def test_round_i8_tensor_pieces(n_peers):
+    """int8 LAMB round whose tensors start inside codec blocks and inside
+    LAMB tiles: several tensors in one block (8-element and empty ones among
+    them), tensors over many blocks, a ragged end; 3 active peers (small
+    peer batch), 9 (full batch) and 70 (two launches chained through the
+    fp32 running sum)."""
+    print(f"\n[i8 pieces] peers={n_peers}", flush=True)
+    rng = np.random.default_rng(8100 + n_peers)
+    sizes = [8, 0, 8, 16, 1000, 0, 4096 + 8, 24, 3 * 4096, 8, 2040, 2 * 4096 + 512, 0, 4088, 8, 5]
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.uint64)
+    P = int(off[-1])
+    counts = rng.integers(1, 300, n_peers).astype(np.uint32)
+    grads = [(rng.standard_normal(P) * 1e-3).astype(F) for _ in range(n_peers)]
+    bounds = oracle.partition(P, 3, rng.integers(1, 1000, 3), 1024)
+    x = (rng.standard_normal(P) * 0.02).astype(F)
+    m = (rng.standard_normal(P) * 1e-4).astype(F)
+    v = np.square(rng.standard_normal(P) * 1e-3).astype(F)
+    cfg = dict(lr=2e-3, beta1=0.9, beta2=0.999, eps=1e-6, weight_decay=0.01, step=3)
+    flags = rng.integers(0, 4, len(sizes)).astype(np.uint8)
+    flags[6] = 3
+    flags[8] = 3
+    _check_round(dict(codec=I8, opt="lamb", off=off, flags=flags, P=P, counts=counts, local=1, grads=grads,
+                      bounds=bounds, x=x, m=m, v=v, cfg=cfg))
+
+
 def _check_round(c):
     codec, P, counts, local = c["codec"], c["P"], c["counts"], c["local"]
     n = len(counts)
