@@ -14,7 +14,8 @@ fails, probability (1 - p)^m, and otherwise restarts, so one iteration takes
 1 / (1 - p)^m attempts in expectation; d(m) = ceil(log_m n) iterations are
 needed.  E(m) = d(m) / (1 - p)^m, minimised over m in [2, n] (m = n is the
 single global group); ties go to the smaller m.  Written as the plain
-enumeration of that definition.
+enumeration of that definition.  Parity unpinned beyond the paper's two
+limits: the model of failures is this reading's, not the paper's.
 """
 
 from __future__ import annotations
