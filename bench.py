@@ -80,7 +80,6 @@ KERNEL_KINDS = {
     "void dedloc::opt_a_kernel<3, 0>": "lamb_a_fused_fp16",
     "void dedloc::opt_a_kernel<4, 0>": "lamb_a_fused_fp16",
     "void dedloc::opt_a_kernel<5, 0>": "lamb_a_fused_fp16",
-    "void dedloc::opt_trust_kernel<0>": "lamb_trust",
     "void dedloc::opt_b_kernel<0, 0>": "lamb_b",
     "void dedloc::opt_a_kernel<0, 1>": "lars_a_f32",
     "void dedloc::opt_a_kernel<1, 1>": "lars_a_fp16",
@@ -88,7 +87,6 @@ KERNEL_KINDS = {
     "void dedloc::opt_a_kernel<3, 1>": "lars_a_fused_fp16",
     "void dedloc::opt_a_kernel<4, 1>": "lars_a_fused_fp16",
     "void dedloc::opt_a_kernel<5, 1>": "lars_a_fused_fp16",
-    "void dedloc::opt_trust_kernel<1>": "lars_trust",
     "void dedloc::opt_b_kernel<0, 1>": "lars_b",
     "void dedloc::opt_b_kernel<1, 1>": "lars_b",
     "void dedloc::opt_b_kernel<2, 1>": "lars_b",

@@ -166,9 +166,12 @@ int dedloc_reduce_shard(const void *const *peer_codes, const float *const *peer_
 /* Workspace for dedloc_lamb_step / dedloc_round (and the LARS
  * counterparts dedloc_lars_step / dedloc_round_lars) with this tensor table
  * (offsets: host, n_tensors+1): two fp64 partial sums per 2048-element tile
- * and one fp32 trust ratio per tensor.  Returns 0 for an invalid table.
- * Its contents need no initialisation and carry nothing between calls;
- * calls that share one workspace must not overlap in time. */
+ * and one 8-byte word per tensor (its trust ratio, tagged with a value that
+ * differs from call to call).  Returns 0 for an invalid table.  Its
+ * contents need no initialisation and carry nothing between calls (a word
+ * left by an earlier call, or by anything else, does not carry the tag of
+ * the current one); calls that share one workspace must not overlap in
+ * time. */
 size_t dedloc_lamb_workspace_bytes(uint64_t P, const uint64_t *offsets, uint32_t n_tensors);
 
 /* Zero-fill a device buffer (for example a workspace) with a kernel: no
@@ -436,6 +439,14 @@ int dedloc_profile_begin(uint32_t max_launches);
 int dedloc_profile_end(uint32_t n_kinds, double *total_ms, uint64_t *launches);
 int dedloc_kernel_kinds(void);
 const char *dedloc_kernel_name(int kind);
+
+/* Test hook of the LAMB and LARS steps and rounds.  Inside the pass that
+ * applies the update, one workgroup per tensor computes the tensor's trust
+ * ratio and publishes it; the others poll for it at most `polls` times
+ * (default 4096), then compute it themselves, in the same order, so the
+ * results are the same bits for every value (0: every workgroup computes
+ * it).  Process-wide, read when a call is made; returns the previous value. */
+uint32_t dedloc_test_trust_polls(uint32_t polls);
 
 #ifdef __cplusplus
 }

@@ -6,8 +6,11 @@
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
+#include <unistd.h>
 
 #include <algorithm>
+#include <atomic>
+#include <chrono>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -45,14 +48,14 @@ bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
 // ------------------------------------------------------------ profiling
 enum Kind {
     K_ENCODE_FP16, K_DECODE_FP16, K_ENCODE_I8, K_DECODE_I8, K_REDUCE_FP16, K_REDUCE_I8,
-    K_LAMB_A_F32, K_LAMB_A_FP16, K_LAMB_A_I8, K_LAMB_A_FUSED_FP16, K_LAMB_TRUST, K_LAMB_B,
-    K_LARS_A_F32, K_LARS_A_FP16, K_LARS_A_I8, K_LARS_A_FUSED_FP16, K_LARS_TRUST, K_LARS_B,
+    K_LAMB_A_F32, K_LAMB_A_FP16, K_LAMB_A_I8, K_LAMB_A_FUSED_FP16, K_LAMB_B,
+    K_LARS_A_F32, K_LARS_A_FP16, K_LARS_A_I8, K_LARS_A_FUSED_FP16, K_LARS_B,
     K_ACCUMULATE, K_FINALIZE_FP16, K_FINALIZE_I8, K_FILL, K_COUNT
 };
 const char *const kKindNames[K_COUNT] = {
     "encode_fp16", "decode_fp16", "encode_i8", "decode_i8", "reduce_fp16", "reduce_i8",
-    "lamb_a_f32", "lamb_a_fp16", "lamb_a_i8", "lamb_a_fused_fp16", "lamb_trust", "lamb_b",
-    "lars_a_f32", "lars_a_fp16", "lars_a_i8", "lars_a_fused_fp16", "lars_trust", "lars_b",
+    "lamb_a_f32", "lamb_a_fp16", "lamb_a_i8", "lamb_a_fused_fp16", "lamb_b",
+    "lars_a_f32", "lars_a_fp16", "lars_a_i8", "lars_a_fused_fp16", "lars_b",
     "accumulate", "finalize_fp16", "finalize_i8", "fill_zero"};
 
 struct Profiler {
@@ -273,7 +276,7 @@ void make_plan(uint64_t P, const uint64_t *off, const uint8_t *flags, uint32_t T
     }
     pl.n_tiles = base_tile;
     pl.ws_partials = round_up((size_t)base_tile * 2 * sizeof(double), 256);
-    pl.ws_trust = round_up((size_t)T * sizeof(float), 256);
+    pl.ws_trust = round_up((size_t)T * sizeof(unsigned long long), 256);
     pl.ws_total = pl.ws_partials + pl.ws_trust;
 }
 
@@ -281,9 +284,13 @@ LambWs carve(const Plan &pl, void *ws) {
     char *b = (char *)ws;
     LambWs w;
     w.partials = (double *)b;
-    w.trust = (float *)(b + pl.ws_partials);
+    w.trust = (unsigned long long *)(b + pl.ws_partials);
     return w;
 }
+
+// Polls of a tensor's published trust ratio in pass B before a workgroup
+// computes it itself (dedloc_test_trust_polls).
+std::atomic<uint32_t> g_trust_polls{4096};
 
 int lamb_params(const dedloc_lamb_cfg *cfg, OptParams &op) {
     if (!cfg) return fail(DEDLOC_ERR_INVALID_ARG, "cfg must not be NULL");
@@ -303,6 +310,7 @@ int lamb_params(const dedloc_lamb_cfg *cfg, OptParams &op) {
     }
     op.eps = cfg->eps;
     op.unit_trust = cfg->force_unit_trust ? 1 : 0;
+    op.trust_polls = g_trust_polls.load(std::memory_order_relaxed);
     return DEDLOC_OK;
 }
 
@@ -314,6 +322,7 @@ int lars_params(const dedloc_lars_cfg *cfg, OptParams &op) {
     op.momentum = cfg->momentum;
     op.trust_coef = cfg->trust_coef;
     op.unit_trust = cfg->force_unit_trust ? 1 : 0;
+    op.trust_polls = g_trust_polls.load(std::memory_order_relaxed);
     return DEDLOC_OK;
 }
 
@@ -342,23 +351,36 @@ int grad_src(int32_t codec) {
     return codec == DEDLOC_CODEC_F32 ? kSrcF32 : codec == DEDLOC_CODEC_FP16 ? kSrcFP16 : kSrcI8;
 }
 
-// Per chunk of tensors: pass A (gradient from src_a), the trust ratios,
-// pass B (LARS reads the gradient again from src_b).
+// A tag that differs from call to call: pass B recognises the trust ratios
+// published during this call by it.  Never 0 or ~0 (the usual contents of
+// fresh memory); the start is drawn from the clock and the process id, so
+// that a workspace left by another process is unlikely to carry it.
+uint32_t next_epoch() {
+    static std::atomic<uint32_t> ctr{(uint32_t)std::chrono::steady_clock::now().time_since_epoch().count() * 2654435761u ^
+                                     (uint32_t)getpid()};
+    for (;;) {
+        const uint32_t e = ctr.fetch_add(1u, std::memory_order_relaxed);
+        if (e != 0u && e != ~0u) return e;
+    }
+}
+
+// Per chunk of tensors: pass A (gradient from src_a) and pass B, which
+// computes the trust ratios (LARS reads the gradient again from src_b).
 int run_opt(int opt, int src_a, int src_b, const Plan &pl, const PeerTable *pt, const GradArgs &ga_a,
             const GradArgs &ga_b, const OptParams &op, float *x, float *m, float *v, void *ws,
             float *trust_out, hipStream_t s) {
     const LambWs w = carve(pl, ws);
     const int k_a = (opt == kOptLamb ? K_LAMB_A_F32 : K_LARS_A_F32) + std::min(src_a, (int)kSrcPeersFP16);
-    const int k_t = opt == kOptLamb ? K_LAMB_TRUST : K_LARS_TRUST;
     const int k_b = opt == kOptLamb ? K_LAMB_B : K_LARS_B;
+    const uint32_t epoch = next_epoch();
     for (size_t c = 0; c < pl.chunks.size(); c++) {
         const Chunk &ch = pl.chunks[c];
         const uint32_t tiles = pl.chunk_tiles[c];
         hipError_t e = timed(k_a, s, [&] { return launch_opt_a(opt, src_a, ch, tiles, pt, ga_a, op, x, m, v, w, s); });
         if (e != hipSuccess) return hip_fail(e, "optimizer pass A launch");
-        e = timed(k_t, s, [&] { return launch_opt_trust(opt, ch, op, w, trust_out, s); });
-        if (e != hipSuccess) return hip_fail(e, "trust-ratio launch");
-        e = timed(k_b, s, [&] { return launch_opt_b(opt, src_b, ch, tiles, ga_b, op, x, m, v, w, s); });
+        e = timed(k_b, s, [&] {
+            return launch_opt_b(opt, src_b, ch, tiles, ga_b, op, x, m, v, w, epoch, trust_out, s);
+        });
         if (e != hipSuccess) return hip_fail(e, "optimizer pass B launch");
     }
     return DEDLOC_OK;
@@ -929,6 +951,8 @@ int dedloc_profile_end(uint32_t n_kinds, double *total_ms, uint64_t *launches) {
     g_prof.used = 0;
     return DEDLOC_OK;
 }
+
+uint32_t dedloc_test_trust_polls(uint32_t polls) { return g_trust_polls.exchange(polls); }
 
 int dedloc_kernel_kinds(void) { return K_COUNT; }
 

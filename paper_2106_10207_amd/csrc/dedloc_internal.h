@@ -113,6 +113,7 @@ struct OptParams {
     float beta1, beta2, omb1, omb2, c1, c2, eps;  // LAMB
     float momentum, trust_coef;                   // LARS
     int32_t unit_trust;
+    uint32_t trust_polls;  // pass B: polls of a tensor's published ratio before computing it
 };
 
 // Where the LAMB step takes its gradient from.
@@ -136,8 +137,8 @@ struct GradArgs {
 };
 
 struct LambWs {
-    double *partials;        // 2 per tile: sum x^2, sum u^2
-    float *trust;            // per tensor: r_t, read by pass B
+    double *partials;            // 2 per tile: sum x^2, sum u^2
+    unsigned long long *trust;   // per tensor: (epoch << 32) | bits of r_t, published inside pass B
 };
 
 // Launchers (return hipError_t of the launch).
@@ -151,11 +152,9 @@ hipError_t launch_reduce_i8(const GroupTable &gt, uint64_t len, const ChainArgs 
 hipError_t launch_opt_a(int opt, int src, const Chunk &ch, uint32_t n_tiles, const PeerTable *pt,
                         const GradArgs &ga, const OptParams &op, float *x, float *m, float *v,
                         const LambWs &ws, hipStream_t s);
-hipError_t launch_opt_trust(int opt, const Chunk &ch, const OptParams &op, const LambWs &ws,
-                            float *trust_out, hipStream_t s);
 hipError_t launch_opt_b(int opt, int src, const Chunk &ch, uint32_t n_tiles, const GradArgs &ga,
-                        const OptParams &op, float *x, float *m, float *v, const LambWs &ws,
-                        hipStream_t s);
+                        const OptParams &op, float *x, float *m, float *v, const LambWs &ws, uint32_t epoch,
+                        float *trust_out, hipStream_t s);
 hipError_t launch_accumulate(float *acc, const void *grad, bool fp16, uint64_t n, float b, hipStream_t s);
 hipError_t launch_finalize_fp16(float *acc, uint64_t n, float count, uint16_t *codes, int reset, hipStream_t s);
 hipError_t launch_finalize_i8(float *acc, uint64_t n, float count, int8_t *codes, float *scales, int reset,

@@ -627,19 +627,16 @@ __global__ __launch_bounds__(kWG) void opt_a_kernel(const Chunk ch, const PeerTa
     }
 }
 
-// Trust ratios of the chunk's tensors: block k sums tensor k's tile partials
-// in a fixed order (lane-strided, then a fixed tree), so r_t is the same on
-// every run.  Empty tensors have both norms 0 and get r = 1.
-//   LAMB: r = ||x|| / ||u||;  LARS: r = eta*||x|| / (||g|| + lambda*||x||).
-template <int OPT>
-__global__ __launch_bounds__(kWG) void opt_trust_kernel(const Chunk ch, const OptParams op,
-                                                        LambWs ws, float *__restrict__ trust_out) {
-    const uint32_t k = blockIdx.x;
+// Sums over tensor k of the chunk of its tile partials (x^2, and u^2 or
+// g^2), in a fixed order: lane-strided, then a fixed tree.  Every thread of
+// the workgroup calls it; thread 0 gets the sums.
+__device__ __forceinline__ void tensor_sums(const Chunk &ch, const LambWs &ws, uint32_t k, double &a0, double &a1) {
     const uint32_t first = ch.tile_base + ch.tile_begin[k];
     const uint32_t ntiles = ch.tile_begin[k + 1] - ch.tile_begin[k];
     typedef double f64x2 __attribute__((ext_vector_type(2)));
     const f64x2 *part = (const f64x2 *)ws.partials + first;
-    double a0 = 0.0, a1 = 0.0;
+    a0 = 0.0;
+    a1 = 0.0;
     constexpr int U = DEDLOC_TRUST_UNROLL;  // loads in flight per lane
     for (uint32_t i0 = 0; i0 < ntiles; i0 += U * kWG) {
         f64x2 q[U];
@@ -655,61 +652,149 @@ __global__ __launch_bounds__(kWG) void opt_trust_kernel(const Chunk ch, const Op
         }
     }
     block_sum2(a0, a1);
-    if (threadIdx.x == 0) {
-        const double X = sqrt(a0), Y = sqrt(a1);
-        float r = 1.0f;
-        if (!op.unit_trust && (ch.flags[k] & 2u) && X > 0.0 && Y > 0.0) {
-            if (OPT == kOptLamb) {
-                r = (float)(X / Y);
-            } else {
-                const double lam = (ch.flags[k] & 1u) ? (double)op.wd : 0.0;
-                r = (float)((double)op.trust_coef * X / (Y + lam * X));
-            }
+}
+
+// The ratio of tensor k from its sums (r = 1 when disabled or a norm is 0).
+//   LAMB: r = ||x|| / ||u||;  LARS: r = eta*||x|| / (||g|| + lambda*||x||).
+template <int OPT>
+__device__ __forceinline__ float trust_ratio(const Chunk &ch, const OptParams &op, uint32_t k, double a0,
+                                             double a1) {
+    const double X = sqrt(a0), Y = sqrt(a1);
+    float r = 1.0f;
+    if (!op.unit_trust && (ch.flags[k] & 2u) && X > 0.0 && Y > 0.0) {
+        if (OPT == kOptLamb) {
+            r = (float)(X / Y);
+        } else {
+            const double lam = (ch.flags[k] & 1u) ? (double)op.wd : 0.0;
+            r = (float)((double)op.trust_coef * X / (Y + lam * X));
         }
-        ws.trust[ch.t0 + k] = r;
-        if (trust_out) trust_out[ch.t0 + k] = r;
     }
+    return r;
+}
+
+// The trust ratio of tensor k inside pass B.  One workgroup of the tensor,
+// the producer (dispatched ahead of every other tile), sums the partials
+// and publishes r in the tensor's workspace word as (epoch << 32 | bits of
+// r) with one relaxed device-scope atomic store; the others poll that word
+// with relaxed device-scope atomic loads until it carries this call's
+// epoch (a value and its tag in one word: no ordering between two
+// locations is needed).  The polling is bounded: a workgroup that gives up
+// sums the partials itself, in the same order, so r is the same bits on
+// every path and every kernel exits.  Every thread calls it.
+template <int OPT>
+__device__ __forceinline__ float tensor_ratio(const Chunk &ch, const OptParams &op, const LambWs &ws,
+                                              uint32_t k, bool producer, uint32_t epoch,
+                                              float *__restrict__ trust_out) {
+    __shared__ float s_r;
+    __shared__ int s_have;
+    unsigned long long *word = ws.trust + ch.t0 + k;
+    if (!producer) {
+        if (threadIdx.x == 0) {
+            int have = 0;
+            unsigned bits = 0u;
+            for (uint32_t i = 0; i < op.trust_polls; i++) {
+                const unsigned long long w = __hip_atomic_load(word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if ((uint32_t)(w >> 32) == epoch) {
+                    have = 1;
+                    bits = (uint32_t)w;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(2);
+            }
+            s_have = have;
+            s_r = __uint_as_float(bits);
+        }
+        __syncthreads();
+        if (s_have) return s_r;  // workgroup-uniform
+    }
+    double a0, a1;
+    tensor_sums(ch, ws, k, a0, a1);
+    if (threadIdx.x == 0) {
+        const float r = trust_ratio<OPT>(ch, op, k, a0, a1);
+        if (producer) {
+            __hip_atomic_store(word, ((unsigned long long)epoch << 32) | __float_as_uint(r), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+            if (trust_out) trust_out[ch.t0 + k] = r;
+        }
+        s_r = r;
+    }
+    __syncthreads();
+    return s_r;
 }
 
 // Pass B.  LAMB: x' = x - (lr * r_t) * u, with u recomputed from x, m', v' by
 // the same operations as pass A.  LARS: v' = fma(mu, v, (lr*r_t)*(g + lambda*x)),
-// x' = x - v', with g read again from the gathered message (SRC).
+// x' = x - v', with g read again from the gathered message (SRC).  The
+// tile's data are loaded and the step direction formed before r_t is known.
 template <int SRC, int OPT>
 __global__ __launch_bounds__(kWG) void opt_b_kernel(const Chunk ch, const GradArgs ga,
                                                     const OptParams op, float *__restrict__ x,
                                                     float *__restrict__ m, float *__restrict__ v,
-                                                    LambWs ws) {
-    const uint32_t b = DEDLOC_B_REVERSE ? gridDim.x - 1 - blockIdx.x : blockIdx.x;
-    const uint32_t k = chunk_tensor(ch, b);
+                                                    LambWs ws, uint32_t epoch, float *__restrict__ trust_out) {
+    // Workgroups [0, nt) are the producers: tile 0 of tensor k = blockIdx.x
+    // (the producer of an empty tensor writes r = 1 and exits).  The rest
+    // cover every tile b of the chunk (last to first when DEDLOC_B_REVERSE:
+    // the re-reads start with what pass A touched last) and skip tile 0.
+    uint32_t k, tile;
+    const bool producer = blockIdx.x < ch.nt;
+    if (producer) {
+        k = blockIdx.x;
+        tile = 0;
+        if (ch.tile_begin[k] == ch.tile_begin[k + 1]) {
+            if (threadIdx.x == 0 && trust_out) trust_out[ch.t0 + k] = 1.0f;
+            return;
+        }
+    } else {
+        const uint32_t q = blockIdx.x - ch.nt;
+        const uint32_t b = DEDLOC_B_REVERSE ? gridDim.x - 1 - ch.nt - q : q;
+        k = chunk_tensor(ch, b);
+        tile = b - ch.tile_begin[k];
+        if (tile == 0) return;
+    }
     const uint64_t t_hi = ch.base + ch.start[k + 1];
-    const uint64_t base = ch.base + ch.start[k] + (uint64_t)(b - ch.tile_begin[k]) * kTile;
+    const uint64_t base = ch.base + ch.start[k] + (uint64_t)tile * kTile;
     const float lam = (ch.flags[k] & 1u) ? op.wd : 0.0f;
-    const float lrr = op.lr * ws.trust[ch.t0 + k];
+    // the producer publishes r_t before touching its own tile (its partial
+    // loads would otherwise queue behind the tile's loads)
+    float lrr = producer ? op.lr * tensor_ratio<OPT>(ch, op, ws, k, true, epoch, trust_out) : 0.0f;
+    float xv[kVPL][8], dv[kVPL][8], vv[kVPL][8];
+    int cnt[kVPL];
 #pragma unroll
     for (int r = 0; r < kVPL; r++) {
         const uint64_t e0 = base + ((uint64_t)r * kWG + threadIdx.x) * kVec;
-        if (e0 >= t_hi) break;
-        const int cnt = (int)(t_hi - e0 < (uint64_t)kVec ? t_hi - e0 : (uint64_t)kVec);
-        float xv[8], vv[8];
-        load8(x, e0, cnt, xv);
-        load8(v, e0, cnt, vv);
+        cnt[r] = e0 < t_hi ? (int)(t_hi - e0 < (uint64_t)kVec ? t_hi - e0 : (uint64_t)kVec) : 0;
+        if (cnt[r] == 0) continue;
+        load8(x, e0, cnt[r], xv[r]);
+        load8(v, e0, cnt[r], vv[r]);
         if (OPT == kOptLamb) {
             float mv[8];
-            load8(m, e0, cnt, mv);
+            load8(m, e0, cnt[r], mv);
 #pragma unroll
-            for (int j = 0; j < 8; j++) xv[j] = xv[j] - lrr * lamb_dir(mv[j], vv[j], xv[j], lam, op);
+            for (int j = 0; j < 8; j++) dv[r][j] = lamb_dir(mv[j], vv[r][j], xv[r][j], lam, op);
         } else {
             float g[8];
-            load_grad<SRC>(ga, PeerTable{}, e0, cnt, g);
+            load_grad<SRC>(ga, PeerTable{}, e0, cnt[r], g);
+#pragma unroll
+            for (int j = 0; j < 8; j++) dv[r][j] = g[j] + lam * xv[r][j];
+        }
+    }
+    if (!producer) lrr = op.lr * tensor_ratio<OPT>(ch, op, ws, k, false, epoch, trust_out);
+#pragma unroll
+    for (int r = 0; r < kVPL; r++) {
+        if (cnt[r] == 0) continue;
+        const uint64_t e0 = base + ((uint64_t)r * kWG + threadIdx.x) * kVec;
+        if (OPT == kOptLamb) {
+#pragma unroll
+            for (int j = 0; j < 8; j++) xv[r][j] = xv[r][j] - lrr * dv[r][j];
+        } else {
 #pragma unroll
             for (int j = 0; j < 8; j++) {
-                const float d = g[j] + lam * xv[j];
-                vv[j] = fmaf(op.momentum, vv[j], lrr * d);
-                xv[j] = xv[j] - vv[j];
+                vv[r][j] = fmaf(op.momentum, vv[r][j], lrr * dv[r][j]);
+                xv[r][j] = xv[r][j] - vv[r][j];
             }
-            store8(v, e0, cnt, vv);
+            store8(v, e0, cnt[r], vv[r]);
         }
-        store8(x, e0, cnt, xv);
+        store8(x, e0, cnt[r], xv[r]);
     }
 }
 
@@ -891,23 +976,17 @@ hipError_t launch_opt_a(int opt, int src, const Chunk &ch, uint32_t n_tiles, con
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_opt_trust(int opt, const Chunk &ch, const OptParams &op, const LambWs &ws,
-                            float *trust_out, hipStream_t s) {
-    if (opt == kOptLamb) DEDLOC_LAUNCH(dim3(ch.nt), opt_trust_kernel<kOptLamb>, s, ch, op, ws, trust_out);
-    if (opt == kOptLars) DEDLOC_LAUNCH(dim3(ch.nt), opt_trust_kernel<kOptLars>, s, ch, op, ws, trust_out);
-    return hipErrorInvalidValue;
-}
-
 hipError_t launch_opt_b(int opt, int src, const Chunk &ch, uint32_t n_tiles, const GradArgs &ga,
-                        const OptParams &op, float *x, float *m, float *v, const LambWs &ws,
-                        hipStream_t s) {
+                        const OptParams &op, float *x, float *m, float *v, const LambWs &ws, uint32_t epoch,
+                        float *trust_out, hipStream_t s) {
+    const dim3 g(ch.nt + n_tiles);  // one producer per tensor, then every tile
     if (opt == kOptLamb)
-        DEDLOC_LAUNCH(dim3(n_tiles), (opt_b_kernel<kSrcF32, kOptLamb>), s, ch, ga, op, x, m, v, ws);
+        DEDLOC_LAUNCH(g, (opt_b_kernel<kSrcF32, kOptLamb>), s, ch, ga, op, x, m, v, ws, epoch, trust_out);
     if (opt != kOptLars) return hipErrorInvalidValue;
     switch (src) {
-    case kSrcF32: DEDLOC_LAUNCH(dim3(n_tiles), (opt_b_kernel<kSrcF32, kOptLars>), s, ch, ga, op, x, m, v, ws);
-    case kSrcFP16: DEDLOC_LAUNCH(dim3(n_tiles), (opt_b_kernel<kSrcFP16, kOptLars>), s, ch, ga, op, x, m, v, ws);
-    case kSrcI8: DEDLOC_LAUNCH(dim3(n_tiles), (opt_b_kernel<kSrcI8, kOptLars>), s, ch, ga, op, x, m, v, ws);
+    case kSrcF32: DEDLOC_LAUNCH(g, (opt_b_kernel<kSrcF32, kOptLars>), s, ch, ga, op, x, m, v, ws, epoch, trust_out);
+    case kSrcFP16: DEDLOC_LAUNCH(g, (opt_b_kernel<kSrcFP16, kOptLars>), s, ch, ga, op, x, m, v, ws, epoch, trust_out);
+    case kSrcI8: DEDLOC_LAUNCH(g, (opt_b_kernel<kSrcI8, kOptLars>), s, ch, ga, op, x, m, v, ws, epoch, trust_out);
     default: return hipErrorInvalidValue;
     }
 }

@@ -141,6 +141,7 @@ _SIGS = {
     "dedloc_profile_begin": ([ctypes.c_uint32], ctypes.c_int),
     "dedloc_profile_end": ([ctypes.c_uint32, ctypes.c_void_p, ctypes.c_void_p], ctypes.c_int),
     "dedloc_kernel_kinds": ([], ctypes.c_int),
+    "dedloc_test_trust_polls": ([ctypes.c_uint32], ctypes.c_uint32),
     "dedloc_kernel_name": ([ctypes.c_int], ctypes.c_char_p),
 }
 
@@ -449,6 +450,13 @@ def dedloc_round_noalloc(peer_codes, counts, bounds, codec: int, x, m, v, offset
 
 def dedloc_profile_begin(max_launches: int = 1 << 16):
     _check(load().dedloc_profile_begin(max_launches))
+
+
+def dedloc_test_trust_polls(polls: int) -> int:
+    """Test hook: how often a workgroup polls for a tensor's published trust
+    ratio before computing it itself (0: always itself); returns the
+    previous value.  Results do not depend on it."""
+    return int(load().dedloc_test_trust_polls(int(polls)))
 
 
 def dedloc_profile_end():
