@@ -165,12 +165,13 @@ int dedloc_reduce_shard(const void *const *peer_codes, const float *const *peer_
 
 /* Workspace for dedloc_lamb_step / dedloc_round (and the LARS
  * counterparts dedloc_lars_step / dedloc_round_lars) with this tensor table
- * (offsets: host, n_tensors+1): two fp64 partial sums per 2048-element tile
- * and one 8-byte word per tensor (its trust ratio, tagged with a value that
- * differs from call to call).  Returns 0 for an invalid table.  Its
- * contents need no initialisation and carry nothing between calls (a word
- * left by an earlier call, or by anything else, does not carry the tag of
- * the current one); calls that share one workspace must not overlap in
+ * (offsets: host, n_tensors+1): two fp64 partial sums per 2048-element tile,
+ * one 8-byte word per tensor (its trust ratio, tagged for the call that
+ * wrote it) and a counter that advances the tag on every call, graph
+ * replays included.  Returns 0 for an invalid table.  Its contents need no
+ * initialisation: a word left by an earlier call on the workspace never
+ * carries the current tag, and other contents match it only by a 2^-32
+ * chance per tensor.  Calls that share one workspace must not overlap in
  * time. */
 size_t dedloc_lamb_workspace_bytes(uint64_t P, const uint64_t *offsets, uint32_t n_tensors);
 

@@ -226,7 +226,7 @@ struct Plan {
     std::vector<Chunk> chunks;
     std::vector<uint32_t> chunk_tiles;
     uint32_t n_tiles = 0;
-    size_t ws_partials = 0, ws_trust = 0, ws_total = 0;
+    size_t ws_partials = 0, ws_trust = 0, ws_epoch = 0, ws_total = 0;
 };
 
 int check_tensors(uint64_t P, const uint64_t *off, uint32_t T) {
@@ -277,7 +277,8 @@ void make_plan(uint64_t P, const uint64_t *off, const uint8_t *flags, uint32_t T
     pl.n_tiles = base_tile;
     pl.ws_partials = round_up((size_t)base_tile * 2 * sizeof(double), 256);
     pl.ws_trust = round_up((size_t)T * sizeof(unsigned long long), 256);
-    pl.ws_total = pl.ws_partials + pl.ws_trust;
+    pl.ws_epoch = 256;
+    pl.ws_total = pl.ws_partials + pl.ws_trust + pl.ws_epoch;
 }
 
 LambWs carve(const Plan &pl, void *ws) {
@@ -285,6 +286,7 @@ LambWs carve(const Plan &pl, void *ws) {
     LambWs w;
     w.partials = (double *)b;
     w.trust = (unsigned long long *)(b + pl.ws_partials);
+    w.epoch = (uint32_t *)(b + pl.ws_partials + pl.ws_trust);
     return w;
 }
 
@@ -351,17 +353,14 @@ int grad_src(int32_t codec) {
     return codec == DEDLOC_CODEC_F32 ? kSrcF32 : codec == DEDLOC_CODEC_FP16 ? kSrcFP16 : kSrcI8;
 }
 
-// A tag that differs from call to call: pass B recognises the trust ratios
-// published during this call by it.  Never 0 or ~0 (the usual contents of
-// fresh memory); the start is drawn from the clock and the process id, so
-// that a workspace left by another process is unlikely to carry it.
-uint32_t next_epoch() {
+// The host's part of the tag of a call's published trust ratios (pass B
+// adds the workspace counter that pass A advances): a process-wide
+// sequence with a start drawn from the clock and the process id, so that
+// workspace contents left by anything else are unlikely to carry it.
+uint32_t next_nonce() {
     static std::atomic<uint32_t> ctr{(uint32_t)std::chrono::steady_clock::now().time_since_epoch().count() * 2654435761u ^
                                      (uint32_t)getpid()};
-    for (;;) {
-        const uint32_t e = ctr.fetch_add(1u, std::memory_order_relaxed);
-        if (e != 0u && e != ~0u) return e;
-    }
+    return ctr.fetch_add(0x9E3779B9u, std::memory_order_relaxed);
 }
 
 // Per chunk of tensors: pass A (gradient from src_a) and pass B, which
@@ -372,14 +371,14 @@ int run_opt(int opt, int src_a, int src_b, const Plan &pl, const PeerTable *pt, 
     const LambWs w = carve(pl, ws);
     const int k_a = (opt == kOptLamb ? K_LAMB_A_F32 : K_LARS_A_F32) + std::min(src_a, (int)kSrcPeersFP16);
     const int k_b = opt == kOptLamb ? K_LAMB_B : K_LARS_B;
-    const uint32_t epoch = next_epoch();
+    const uint32_t nonce = next_nonce();
     for (size_t c = 0; c < pl.chunks.size(); c++) {
         const Chunk &ch = pl.chunks[c];
         const uint32_t tiles = pl.chunk_tiles[c];
         hipError_t e = timed(k_a, s, [&] { return launch_opt_a(opt, src_a, ch, tiles, pt, ga_a, op, x, m, v, w, s); });
         if (e != hipSuccess) return hip_fail(e, "optimizer pass A launch");
         e = timed(k_b, s, [&] {
-            return launch_opt_b(opt, src_b, ch, tiles, ga_b, op, x, m, v, w, epoch, trust_out, s);
+            return launch_opt_b(opt, src_b, ch, tiles, ga_b, op, x, m, v, w, nonce, trust_out, s);
         });
         if (e != hipSuccess) return hip_fail(e, "optimizer pass B launch");
     }

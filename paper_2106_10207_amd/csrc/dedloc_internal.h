@@ -139,6 +139,7 @@ struct GradArgs {
 struct LambWs {
     double *partials;            // 2 per tile: sum x^2, sum u^2
     unsigned long long *trust;   // per tensor: (epoch << 32) | bits of r_t, published inside pass B
+    uint32_t *epoch;             // the tag of the current launch: advanced by pass A, read by pass B
 };
 
 // Launchers (return hipError_t of the launch).
@@ -153,7 +154,7 @@ hipError_t launch_opt_a(int opt, int src, const Chunk &ch, uint32_t n_tiles, con
                         const GradArgs &ga, const OptParams &op, float *x, float *m, float *v,
                         const LambWs &ws, hipStream_t s);
 hipError_t launch_opt_b(int opt, int src, const Chunk &ch, uint32_t n_tiles, const GradArgs &ga,
-                        const OptParams &op, float *x, float *m, float *v, const LambWs &ws, uint32_t epoch,
+                        const OptParams &op, float *x, float *m, float *v, const LambWs &ws, uint32_t nonce,
                         float *trust_out, hipStream_t s);
 hipError_t launch_accumulate(float *acc, const void *grad, bool fp16, uint64_t n, float b, hipStream_t s);
 hipError_t launch_finalize_fp16(float *acc, uint64_t n, float count, uint16_t *codes, int reset, hipStream_t s);

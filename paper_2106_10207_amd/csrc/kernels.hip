@@ -624,6 +624,9 @@ __global__ __launch_bounds__(kWG) void opt_a_kernel(const Chunk ch, const PeerTa
     if (threadIdx.x == 0) {
         ws.partials[2 * (ch.tile_base + b)] = s0;
         ws.partials[2 * (ch.tile_base + b) + 1] = s1;
+        // a fresh tag for the ratios pass B publishes (the only access to
+        // this word during the launch; pass B reads it after the launch)
+        if (b == 0) ws.epoch[0] = ws.epoch[0] + 1u;
     }
 }
 
@@ -676,9 +679,13 @@ __device__ __forceinline__ float trust_ratio(const Chunk &ch, const OptParams &o
 // the producer (dispatched ahead of every other tile), sums the partials
 // and publishes r in the tensor's workspace word as (epoch << 32 | bits of
 // r) with one relaxed device-scope atomic store; the others poll that word
-// with relaxed device-scope atomic loads until it carries this call's
+// with relaxed device-scope atomic loads until it carries this launch's
 // epoch (a value and its tag in one word: no ordering between two
-// locations is needed).  The polling is bounded: a workgroup that gives up
+// locations is needed).  The epoch is a workspace counter that pass A
+// advances on every launch plus a value the host draws for every call, so
+// every call, graph replays included, has a tag that no word left by an
+// earlier call on this workspace carries (and that other contents match
+// only by a 2^-32 chance).  The polling is bounded: a workgroup that gives up
 // sums the partials itself, in the same order, so r is the same bits on
 // every path and every kernel exits.  Every thread calls it.
 template <int OPT>
@@ -730,7 +737,7 @@ template <int SRC, int OPT>
 __global__ __launch_bounds__(kWG) void opt_b_kernel(const Chunk ch, const GradArgs ga,
                                                     const OptParams op, float *__restrict__ x,
                                                     float *__restrict__ m, float *__restrict__ v,
-                                                    LambWs ws, uint32_t epoch, float *__restrict__ trust_out) {
+                                                    LambWs ws, uint32_t nonce, float *__restrict__ trust_out) {
     // Workgroups [0, nt) are the producers: tile 0 of tensor k = blockIdx.x
     // (the producer of an empty tensor writes r = 1 and exits).  The rest
     // cover every tile b of the chunk (last to first when DEDLOC_B_REVERSE:
@@ -754,6 +761,7 @@ __global__ __launch_bounds__(kWG) void opt_b_kernel(const Chunk ch, const GradAr
     const uint64_t t_hi = ch.base + ch.start[k + 1];
     const uint64_t base = ch.base + ch.start[k] + (uint64_t)tile * kTile;
     const float lam = (ch.flags[k] & 1u) ? op.wd : 0.0f;
+    const uint32_t epoch = ws.epoch[0] + nonce;  // ws.epoch: advanced by this chunk's pass A
     // the producer publishes r_t before touching its own tile (its partial
     // loads would otherwise queue behind the tile's loads)
     float lrr = producer ? op.lr * tensor_ratio<OPT>(ch, op, ws, k, true, epoch, trust_out) : 0.0f;
@@ -977,16 +985,16 @@ hipError_t launch_opt_a(int opt, int src, const Chunk &ch, uint32_t n_tiles, con
 }
 
 hipError_t launch_opt_b(int opt, int src, const Chunk &ch, uint32_t n_tiles, const GradArgs &ga,
-                        const OptParams &op, float *x, float *m, float *v, const LambWs &ws, uint32_t epoch,
+                        const OptParams &op, float *x, float *m, float *v, const LambWs &ws, uint32_t nonce,
                         float *trust_out, hipStream_t s) {
     const dim3 g(ch.nt + n_tiles);  // one producer per tensor, then every tile
     if (opt == kOptLamb)
-        DEDLOC_LAUNCH(g, (opt_b_kernel<kSrcF32, kOptLamb>), s, ch, ga, op, x, m, v, ws, epoch, trust_out);
+        DEDLOC_LAUNCH(g, (opt_b_kernel<kSrcF32, kOptLamb>), s, ch, ga, op, x, m, v, ws, nonce, trust_out);
     if (opt != kOptLars) return hipErrorInvalidValue;
     switch (src) {
-    case kSrcF32: DEDLOC_LAUNCH(g, (opt_b_kernel<kSrcF32, kOptLars>), s, ch, ga, op, x, m, v, ws, epoch, trust_out);
-    case kSrcFP16: DEDLOC_LAUNCH(g, (opt_b_kernel<kSrcFP16, kOptLars>), s, ch, ga, op, x, m, v, ws, epoch, trust_out);
-    case kSrcI8: DEDLOC_LAUNCH(g, (opt_b_kernel<kSrcI8, kOptLars>), s, ch, ga, op, x, m, v, ws, epoch, trust_out);
+    case kSrcF32: DEDLOC_LAUNCH(g, (opt_b_kernel<kSrcF32, kOptLars>), s, ch, ga, op, x, m, v, ws, nonce, trust_out);
+    case kSrcFP16: DEDLOC_LAUNCH(g, (opt_b_kernel<kSrcFP16, kOptLars>), s, ch, ga, op, x, m, v, ws, nonce, trust_out);
+    case kSrcI8: DEDLOC_LAUNCH(g, (opt_b_kernel<kSrcI8, kOptLars>), s, ch, ga, op, x, m, v, ws, nonce, trust_out);
     default: return hipErrorInvalidValue;
     }
 }

@@ -221,7 +221,8 @@ def test_round_noalloc_validation_before_launch():
 def _ws_expected(sizes, tile=2048):
     tiles = sum((n + tile - 1) // tile for n in sizes)
     r = lambda v: (v + 255) // 256 * 256
-    return r(tiles * 16) + r(len(sizes) * 8)  # two fp64 sums per tile, one tagged 8-byte ratio per tensor
+    # two fp64 sums per tile, one tagged 8-byte ratio per tensor, the tag counter
+    return r(tiles * 16) + r(len(sizes) * 8) + 256
 
 
 @pytest.mark.parametrize("sizes", [

@@ -5,7 +5,8 @@
   once, each result still equals the oracle.
 * A round captured into a HIP graph and replayed several times, with eager
   work and synchronisation between replays, gives the eager result every
-  time (the library records only kernel launches)."""
+  time (the library records only kernel launches), also when the replays
+  are consecutive steps whose trust ratios differ."""
 
 import numpy as np
 import pytest
@@ -76,4 +77,44 @@ def test_round_in_graph_replays(idx):
         got = [_np(t).copy() for t in (dr.out_codes, dr.x, dr.m, dr.v, dr.trust)]
         for a, b in zip(got, ref):
             assert np.array_equal(a.view(np.uint8), b.view(np.uint8))
+        _ = torch.ones(1024, device=DEV).sum().item()  # eager work between replays
+
+
+@pytest.mark.parametrize("idx", [0, 3])
+def test_round_in_graph_consecutive_steps(idx):
+    """Replays of a captured round as consecutive optimizer steps (the state
+    evolves, so every replay has other trust ratios): every replay equals
+    the eager round run on the same state, bit for bit.  Each replay's
+    ratios carry a tag of their own although the captured kernel arguments
+    are the same."""
+    print(f"\n[graph steps] {SMALL[idx].name}", flush=True)
+    dr = H.DeviceRound(SMALL[idx], DEV)
+    state0 = [t.clone() for t in (dr.x, dr.m, dr.v)]
+
+    def reset():
+        for t, t0 in zip((dr.x, dr.m, dr.v), state0):
+            t.copy_(t0)
+
+    def outs():
+        return [_np(t).copy() for t in (dr.out_codes, dr.x, dr.m, dr.v, dr.trust)]
+
+    reset()
+    ref = []
+    for _ in range(4):
+        dr.run()
+        ref.append(outs())
+    assert not np.array_equal(ref[0][4], ref[1][4])  # the ratios change from step to step
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    reset()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g, stream=s):
+        dr.call(stream=s)
+    reset()
+    torch.cuda.synchronize()
+    for step in range(4):
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(outs(), ref[step]):
+            assert np.array_equal(a.view(np.uint8), b.view(np.uint8)), step
         _ = torch.ones(1024, device=DEV).sum().item()  # eager work between replays
