@@ -169,7 +169,9 @@ def _kernel_source_digest():
 def summarize_trace(root_dir, workload, extra=""):
     """Average, minimum and maximum duration and call count of every library
     kernel instance from a rocprofv3 --kernel-trace --stats run, with the
-    hash of the kernel source it was taken with."""
+    hash of the kernel source it was taken with; with the run's per-dispatch
+    trace beside it, also the median duration (the run also times the cold
+    steps, a third of the launches, which the median leaves out)."""
     import csv
     rows = {}
     for r in csv.DictReader(open(os.path.join(root_dir, "run_kernel_stats.csv"))):
@@ -179,6 +181,16 @@ def summarize_trace(root_dir, workload, extra=""):
         rows[name] = {"calls": int(r["Calls"]), "avg_us": float(r["AverageNs"]) / 1e3,
                       "min_us": float(r["MinNs"]) / 1e3, "max_us": float(r["MaxNs"]) / 1e3,
                       "kind": KERNEL_KINDS.get(name)}
+    trace = os.path.join(root_dir, "run_kernel_trace.csv")
+    if os.path.exists(trace):
+        durs = {}
+        for r in csv.DictReader(open(trace)):
+            name = r["Kernel_Name"].split("(")[0]
+            if name in rows:
+                durs.setdefault(name, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+        for name, d in durs.items():
+            if len(d) == rows[name]["calls"]:
+                rows[name]["median_us"] = float(np.median(d))
     root = os.path.dirname(os.path.abspath(__file__))
     rec = {"workload": workload, "command": TRACE_COMMAND.format(w=workload, extra=extra),
            "kernels": rows, "kernels_hip_sha256": _kernel_source_digest()}
@@ -198,20 +210,21 @@ def _instance(kind, dr):
     return names.get(kind)
 
 
-def rocprof_average_us(kind, dr):
-    """The committed rocprofv3 average duration of the step's `kind` kernel
-    for this workload, or (None, why) when there is none or the kernel
-    source changed since."""
+def rocprof_durations_us(kind, dr):
+    """The committed rocprofv3 average and median durations of the step's
+    `kind` kernel for this workload (median None when not recorded), or
+    (None, None, why) when there is no summary or the kernel source changed
+    since."""
     root = os.path.dirname(os.path.abspath(__file__))
     path = os.path.join(root, "profiles", f"kernel_stats_{dr.wl.name}.json")
     if not os.path.exists(path):
-        return None, None
+        return None, None, None
     rec = json.load(open(path))
     rel = os.path.relpath(path, root)
     if rec.get("kernels_hip_sha256") != _kernel_source_digest():
-        return None, rel + " (stale: kernel source changed)"
+        return None, None, rel + " (stale: kernel source changed)"
     k = rec["kernels"].get(_instance(kind, dr))
-    return (k["avg_us"], rel) if k else (None, rel)
+    return (k["avg_us"], k.get("median_us"), rel) if k else (None, None, rel)
 
 
 def kernel_roofline(dr, prof, steps):
@@ -273,8 +286,13 @@ def kernel_roofline(dr, prof, steps):
         strict = nbytes - loc * P / per_step
         roof["round_bytes_per_launch"] = strict
         roof["frac_round_bytes"] = round(strict / (avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4)
-    rp_us, rp_src = rocprof_average_us(name, dr)
-    roof["rocprof_avg_launch_us"] = None if rp_us is None else round(rp_us, 2)
+    rp_avg, rp_med, rp_src = rocprof_durations_us(name, dr)
+    roof["rocprof_avg_launch_us"] = None if rp_avg is None else round(rp_avg, 2)
+    roof["rocprof_median_launch_us"] = None if rp_med is None else round(rp_med, 2)
+    # the trace also times the cold-cache steps; with one launch per step its
+    # median is the warm launch the events above time (launch chunks of
+    # unequal size, several per step, compare by the average)
+    rp_us = rp_med if rp_med is not None and per_step == 1 else rp_avg
     roof["frac_rocprof"] = None if rp_us is None else round(nbytes / (rp_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
     roof["rocprof_source"] = rp_src
     return name, roof, {k: _kernel_entry(v, steps, per_launch.get(k)) for k, v in prof.items()}
