@@ -121,6 +121,20 @@ def test_random_round(seed):
     _check_round(c)
 
 
+@pytest.mark.parametrize("seed", range(0, 300, 6))
+def test_random_round_without_published_ratios(seed):
+    """The same rounds with every workgroup of the update pass computing its
+    tensor's trust ratio itself (no polling for the published one)."""
+    c = _case(seed)
+    print(f"\n[seed {seed}, no polls] codec={c['codec']} opt={c['opt']} P={c['P']} tensors={len(c['flags'])}",
+          flush=True)
+    old = D.dedloc_test_trust_polls(0)
+    try:
+        _check_round(c)
+    finally:
+        D.dedloc_test_trust_polls(old)
+
+
 def _degenerate(name, codec, opt):
     """Edge cases of the round: an empty vector, a vector shorter than one
     lane's vector, one peer, an empty shard, all-zero gradients (int8 scale
