@@ -267,7 +267,7 @@ struct Ldl {
 // a dense symmetric system over the coupling rows and D.  Iterative
 // refinement on the unreduced system cleans up the rounding.
 class Kkt {
-    static constexpr int kMaxG = 8;  // dense unknowns one block touches (6 in this program)
+    static constexpr int kMaxG = 6;  // dense unknowns one block touches (6 in this program)
 
   public:
     explicit Kkt(const Lp &lp) : lp_(lp) {
@@ -283,8 +283,13 @@ class Kkt {
         ldl_.reserve();
         theta_.assign(lp.nv, 0.0);
         loc_.resize(lp.blocks.size());
-        for (size_t bi = 0; bi < lp.blocks.size(); bi++) setup(lp.blocks[bi], loc_[bi]);
+        coef_.resize(lp.blocks.size());
+        for (size_t bi = 0; bi < lp.blocks.size(); bi++) setup(lp.blocks[bi], loc_[bi], coef_[bi]);
     }
+
+    // False when a block touched more dense unknowns than kMaxG (the
+    // program's structure allows 6); the system is then not set up.
+    bool ok() const { return ok_; }
 
     void factor(const std::vector<double> &tinv, const std::vector<double> &e) {
         tinv_ = &tinv;
@@ -325,13 +330,14 @@ class Kkt {
         for (size_t bi = 0; bi < lp_.blocks.size(); bi++) {
             const Lp::Block &B = lp_.blocks[bi];
             Local &L = loc_[bi];
+            const Coef &C = coef_[bi];
             const double th[2] = {theta_[B.var[0]], B.nvar > 1 ? theta_[B.var[1]] : 0.0};
             double K[3][3] = {{0}};
             for (int t = 0; t < B.nrow; t++) {
                 K[t][t] = e[B.row[t]];
                 for (int u = 0; u <= t; u++)
-                    for (int v = 0; v < B.nvar; v++) K[t][u] += th[v] * L.arv[t][v] * L.arv[u][v];
-                for (int g = 0; g < L.ng; g++) L.w[t][g] = L.cst[t][g] + th[0] * L.cv[t][g][0] + th[1] * L.cv[t][g][1];
+                    for (int v = 0; v < B.nvar; v++) K[t][u] += th[v] * C.arv[t][v] * C.arv[u][v];
+                for (int g = 0; g < L.ng; g++) L.w[t][g] = C.cst[t][g] + th[0] * C.cv[t][g][0] + th[1] * C.cv[t][g][1];
             }
             L.factor(K, B.nrow);
             double kw[3][kMaxG];  // K^-1 W
@@ -386,15 +392,20 @@ class Kkt {
     }
 
   private:
-    // A block's local rows: their coefficients on the block's variables, the
-    // dense unknowns they couple to (W = cst + theta_0 cv_0 + theta_1 cv_1:
-    // -A_D entries, and through a block variable the coupling rows it is in),
-    // and the factor of their N block.
-    struct Local {
+    // A block's local rows, in two records: what every solve reads (the
+    // dense unknowns they couple to, W = cst + theta_0 cv_0 + theta_1 cv_1 for
+    // the current theta, and the factor of their N block) and what only the
+    // factorisation reads (their coefficients on the block's variables, and
+    // W's parts: -A_D entries, and through a block variable the coupling rows
+    // it is in).  Kept apart, the solves stream a third of the bytes.
+    struct Coef {
         double arv[3][2];
+        double cst[3][kMaxG], cv[3][kMaxG][2];
+    };
+    struct Local {
         int ng = 0;
         int pos[kMaxG];
-        double cst[3][kMaxG], cv[3][kMaxG][2], w[3][kMaxG];
+        double w[3][kMaxG];
         double l[3][3], dg[3];
         void factor(double K[3][3], int m) {
             double dmax = 0.0;
@@ -417,32 +428,44 @@ class Kkt {
             for (int i = m - 1; i >= 0; i--)
                 for (int k = i + 1; k < m; k++) x[i] -= l[k][i] * x[k];
         }
-        int slot(int p) {
+        int slot(int p, Coef &c) {  // -1: more than kMaxG dense unknowns
             for (int g = 0; g < ng; g++)
                 if (pos[g] == p) return g;
+            if (ng == kMaxG) return -1;
             pos[ng] = p;
-            for (int t = 0; t < 3; t++) cst[t][ng] = cv[t][ng][0] = cv[t][ng][1] = 0.0;
+            for (int t = 0; t < 3; t++) c.cst[t][ng] = c.cv[t][ng][0] = c.cv[t][ng][1] = 0.0;
             return ng++;
         }
     };
 
-    void setup(const Lp::Block &B, Local &L) {
+    void setup(const Lp::Block &B, Local &L, Coef &C) {
         L.ng = 0;
         for (int t = 0; t < B.nrow; t++) {
             const int r = B.row[t];
-            for (int v = 0; v < 2; v++) L.arv[t][v] = 0.0;
+            for (int v = 0; v < 2; v++) C.arv[t][v] = 0.0;
             for (int k = lp_.rp[r]; k < lp_.rp[r + 1]; k++) {
                 const int j = lp_.rc[k];
                 if (pos_var_[j] >= 0) {
-                    L.cst[t][L.slot(pos_var_[j])] += -lp_.rv[k];  // -A_D
+                    const int g = L.slot(pos_var_[j], C);
+                    if (g < 0) {
+                        ok_ = false;
+                        return;
+                    }
+                    C.cst[t][g] += -lp_.rv[k];  // -A_D
                     continue;
                 }
                 for (int v = 0; v < B.nvar; v++)
                     if (B.var[v] == j) {
-                        L.arv[t][v] = lp_.rv[k];
+                        C.arv[t][v] = lp_.rv[k];
                         for (int q = lp_.cp[j]; q < lp_.cp[j + 1]; q++) {
                             const int pr = pos_row_[lp_.cr[q]];
-                            if (pr >= 0) L.cv[t][L.slot(pr)][v] += lp_.rv[k] * lp_.cv[q];
+                            if (pr < 0) continue;
+                            const int g = L.slot(pr, C);
+                            if (g < 0) {
+                                ok_ = false;
+                                return;
+                            }
+                            C.cv[t][g][v] += lp_.rv[k] * lp_.cv[q];
                         }
                     }
             }
@@ -507,6 +530,8 @@ class Kkt {
     Ldl ldl_;
     std::vector<double> theta_, rr_, u_, ex_, ey_, cx_, cy_;
     std::vector<Local> loc_;
+    std::vector<Coef> coef_;
+    bool ok_ = true;
     const std::vector<double> *tinv_ = nullptr, *e_ = nullptr;
 };
 
@@ -546,6 +571,7 @@ int interior_point(const Lp &lp, std::vector<double> &x, int *iterations) {
     const int ncomp = nv + nr + (int)std::count(hasub.begin(), hasub.end(), 1);
 
     Kkt kkt(lp);
+    if (!kkt.ok()) return 1;
     std::vector<double> rp(nr), rd(nv), tinv(nv), e(nr), rhs_d(nv), rhs_p(nr);
     std::vector<double> dx, dy, dz(nv), ds(nv), dq(nv), dw(nr);
     std::vector<double> ax_(nv), ay_(nr), az_(nv), as_(nv), aq_(nv), aw_(nr);  // affine direction
