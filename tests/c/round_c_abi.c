@@ -258,6 +258,37 @@ static void device_round(int32_t codec, int local) {
     printf("c-abi %s round%s: P=%llu, %d tensors, %d peers: %s\n", codec == DEDLOC_CODEC_FP16 ? "fp16" : "int8",
            local >= 0 ? " (local peer)" : "", (unsigned long long)P, T, N, failures ? "MISMATCH" : "ok");
 
+    /* the same round from the same state through the entry point without a
+     * workspace argument: the same bits */
+    HIP(hipMemcpy(d_x, x, P * 4, hipMemcpyHostToDevice));
+    HIP(hipMemcpy(d_m, m, P * 4, hipMemcpyHostToDevice));
+    HIP(hipMemcpy(d_v, v, P * 4, hipMemcpyHostToDevice));
+    if (local >= 0) HIP(hipMemset(d_codes[local], 0x7e, P * cb));
+    rc = dedloc_round_noalloc((const void *const *)d_codes, psc, counts, N, bounds, 3, codec, block, d_out,
+                              codec == DEDLOC_CODEC_I8 ? d_out_sc : NULL, d_x, d_m, d_v, P, off, flags, T, &cfg,
+                              d_trust, d_mean, local >= 0 ? &lp : NULL, NULL);
+    CHECK(rc == DEDLOC_OK, "round_noalloc: %d %s", rc, dedloc_last_error());
+    HIP(hipDeviceSynchronize());
+    {
+        void *n_out = malloc(P * cb);
+        float *n_x = malloc(P * 4), *n_m = malloc(P * 4), *n_v = malloc(P * 4), *n_trust = malloc(T * 4);
+        host_copy(n_out, d_out, P * cb);
+        host_copy(n_x, d_x, P * 4);
+        host_copy(n_m, d_m, P * 4);
+        host_copy(n_v, d_v, P * 4);
+        host_copy(n_trust, d_trust, T * 4);
+        CHECK(same_bits(n_out, g_out, P * cb) && same_bits(n_x, gx, P * 4) && same_bits(n_m, gm, P * 4) &&
+                  same_bits(n_v, gv, P * 4) && same_bits(n_trust, g_trust, T * 4),
+              "dedloc_round_noalloc differs from dedloc_round");
+        printf("c-abi %s round%s without a workspace argument: %s\n", codec == DEDLOC_CODEC_FP16 ? "fp16" : "int8",
+               local >= 0 ? " (local peer)" : "", failures ? "MISMATCH" : "ok");
+        free(n_out);
+        free(n_x);
+        free(n_m);
+        free(n_v);
+        free(n_trust);
+    }
+
     for (int p = 0; p < N; p++) {
         HIP(hipFree(d_codes[p]));
         HIP(hipFree(d_scales[p]));

@@ -45,4 +45,6 @@ def test_c_abi_rounds_on_device():
     r = _run()
     print(r.stdout, flush=True)
     assert r.returncode == 0, r.stdout + r.stderr
-    assert r.stdout.count(": ok") == 5, r.stdout
+    # host checks, then four rounds (fp16 / int8, with and without the local
+    # peer), each also through dedloc_round_noalloc
+    assert r.stdout.count(": ok") == 9, r.stdout
